@@ -1,0 +1,27 @@
+"""CPU oracle for group decode attention over a paged KV cache.
+
+TEST INFRASTRUCTURE ONLY. Only ``tests/``, ``__graft_entry__.smoke()`` and the
+CPU-baseline leg of ``bench.py`` may import or call anything in this package;
+the library's product path never does. It shares no code with the HIP library.
+
+Everything is computed in float64 from the plain definitions:
+
+* attention per sequence: ``out = softmax(sigma * q K^T) V`` over the keys of the
+  sequence's group prefix followed by its own response (the GRPO group shares one
+  prompt, Section 2.1 of the paper; the key order is irrelevant mathematically);
+* the log-sum-exp merge of partial results over disjoint key subsets;
+* the KV append (bf16 copy, or OCP e4m3fn quantisation with a per-(page, head)
+  scale);
+* bf16 and OCP e4m3fn decoding from the formats' bit definitions.
+
+Every function here is pinned by ``-m "not gpu"`` tests against library
+routines, closed forms, invariants and brute force; none is "parity unpinned".
+"""
+from .formats import bf16_to_f64, bf16_to_f32, e4m3_to_f64, e4m3_encode, E4M3_MAX
+from .attention import decode_attention, key_slots, attention_for_workload
+from .combine import lse_combine
+from .append import kv_append, append_for_workload
+
+__all__ = ["bf16_to_f64", "bf16_to_f32", "e4m3_to_f64", "e4m3_encode", "E4M3_MAX",
+           "decode_attention", "key_slots", "attention_for_workload",
+           "lse_combine", "kv_append", "append_for_workload"]

@@ -1,0 +1,10 @@
+"""Seeded synthetic inputs for group decode attention.
+
+This package only draws random inputs and lays them out in the paged-KV form
+that both the CPU oracle and the HIP library consume. It performs none of the
+attention arithmetic, so it can be shared by both sides without coupling them.
+"""
+from .configs import CONFIGS, config_by_id
+from .gen import Workload, make_config_workload, make_workload
+
+__all__ = ["CONFIGS", "config_by_id", "Workload", "make_config_workload", "make_workload"]
