@@ -1,0 +1,189 @@
+/*
+ * rp.h - group decode attention over a paged, group-shared KV cache (gfx950).
+ *
+ * The operation is the attention step of autoregressive rollout decoding. In
+ * GRPO rollouts every prompt is sampled K times and the K responses of a prompt
+ * form a group (paper, Section 2.1 and Section 5.1 with K = 8); the decode
+ * workers of the serving engine generate all of them under fixed weights
+ * (Section 4, rollout node). Here a group's prompt-prefix KV is stored once and
+ * every response of the group adds its own ragged response KV.
+ *
+ * For sequence s in group g = seq_to_group[s] and query head j the result is
+ * the plain softmax attention over the concatenated keys
+ *     prefix tokens t < prefix_lens[g]  at page prefix_block_table[g][t / ps], row t % ps
+ *     response tokens t < resp_lens[s]  at page resp_block_table[s][t / ps],   row t % ps
+ * namely, with sigma = softmax_scale and kv-head h = j / (Hq / Hkv):
+ *     s_t = sigma * <q[s][j], k_t[h]>,  lse = ln sum_t exp(s_t),
+ *     out[s][j] = sum_t exp(s_t - lse) * v_t[h].
+ * An empty key set yields out = 0 and lse = -inf.
+ *
+ * Conventions for every call:
+ *  - Pointers inside rp_paged_kv / rp_group_layout and all array arguments are
+ *    DEVICE pointers unless marked "host". The two structs themselves live in
+ *    host memory and are read during the call only.
+ *  - Calls are asynchronous on `stream` (may be NULL for the default stream),
+ *    never synchronise (except rp_validate_layout) and never allocate device
+ *    memory (except rp_validate_layout). The caller owns every buffer.
+ *  - Scalar/pointer arguments are validated synchronously; a failed check
+ *    returns an error before anything is launched. Device array CONTENTS are
+ *    not validated on the hot path: out-of-range page ids or lengths beyond the
+ *    table widths are undefined behaviour (check them with rp_validate_layout).
+ *  - Errors are reported by return code; rp_last_error() gives detail text for
+ *    the calling thread.
+ */
+#ifndef RP_H_
+#define RP_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ihipStream_t* hipStream_t; /* identical to HIP's own typedef */
+
+typedef enum {
+  RP_OK = 0,
+  RP_ERR_INVALID_ARG = 1,  /* null pointer, misalignment, inconsistent sizes */
+  RP_ERR_UNSUPPORTED = 2,  /* valid but not implemented (head_dim, page_size, ratio) */
+  RP_ERR_WORKSPACE = 3,    /* workspace missing or smaller than required */
+  RP_ERR_HIP = 4,          /* a HIP launch or runtime call failed; see rp_last_error */
+  RP_ERR_LAYOUT = 5        /* rp_validate_layout found an out-of-range entry */
+} rp_status;
+
+typedef enum {
+  RP_KV_BF16 = 0,          /* bf16 K/V elements */
+  RP_KV_FP8_E4M3 = 1       /* OCP FP8 e4m3fn codes (max 448, no inf) with fp32 scales */
+} rp_kv_dtype;
+
+/* Paged KV pool, caller-owned.
+ * k_pages, v_pages: [num_pages][num_kv_heads][page_size][head_dim] elements of
+ *   kv_dtype, 16-byte aligned. One (page, kv-head) block is contiguous.
+ * k_scale, v_scale: fp32 [num_pages][num_kv_heads]; element value = decoded
+ *   code * scale of its (page, kv-head). Must be NULL for RP_KV_BF16 and
+ *   non-NULL for RP_KV_FP8_E4M3.
+ * Supported: page_size == 16, head_dim in {64, 128}. */
+typedef struct {
+  void* k_pages;
+  void* v_pages;
+  float* k_scale;
+  float* v_scale;
+  int32_t num_pages;
+  int32_t num_kv_heads;
+  int32_t page_size;
+  int32_t head_dim;
+  rp_kv_dtype kv_dtype;
+} rp_paged_kv;
+
+/* Batch layout: S sequences in num_groups prompt groups, caller-owned int32
+ * device arrays.
+ * seq_to_group[S]                          group of each sequence, in [0, num_groups)
+ * prefix_lens[num_groups]                  shared prompt-prefix tokens per group
+ * prefix_block_table[num_groups][max_prefix_pages]
+ * resp_lens[S]                             response tokens of each sequence
+ * resp_block_table[S][max_resp_pages]
+ * Requires num_q_heads % num_kv_heads == 0 with ratio in {1, 2, 4, 8};
+ * query head j uses kv-head j / (num_q_heads / num_kv_heads). */
+typedef struct {
+  int32_t num_seqs;
+  int32_t num_groups;
+  int32_t num_q_heads;
+  const int32_t* seq_to_group;
+  const int32_t* prefix_lens;
+  const int32_t* prefix_block_table;
+  int32_t max_prefix_pages;
+  const int32_t* resp_lens;
+  const int32_t* resp_block_table;
+  int32_t max_resp_pages;
+} rp_group_layout;
+
+/* Static description of an error code (never NULL). */
+const char* rp_status_string(rp_status status);
+
+/* Detail text of the last error returned on the calling thread ("" if none). */
+const char* rp_last_error(void);
+
+/* KV append: write one new token per sequence.
+ * k_new, v_new: bf16 [num_seqs][num_kv_heads][head_dim], 16-byte aligned.
+ * layout->resp_lens holds the PRE-append lengths L_s; the token goes to
+ * response slot L_s (page resp_block_table[s][L_s / 16], row L_s % 16), which
+ * the caller must have provided in the table. resp_lens is not modified: the
+ * caller advances it. Repeating a call with the same inputs is idempotent.
+ * RP_KV_BF16: the bf16 values are copied.
+ * RP_KV_FP8_E4M3, per (sequence, kv-head), separately for K and V, in fp32:
+ * amax = max|x|; row 0 of a page sets scale = amax / 448 (1 if amax == 0);
+ * a later row keeps the scale if amax <= 448 * scale, otherwise sets
+ * scale = amax / 448 and requantises rows 0..r-1 from code * old_scale; the
+ * row is stored as e4m3(x / scale), round to nearest even, saturated at 448.
+ * Two sequences must not append into the same (page, kv-head). */
+rp_status rp_kv_append(const rp_paged_kv* kv, const rp_group_layout* layout,
+                       const void* k_new, const void* v_new, hipStream_t stream);
+
+/* Workspace bytes needed by rp_group_decode_attn / rp_plan for this shape.
+ * Depends only on host-side scalars (S, num_groups, Hq, Hkv, head_dim,
+ * max_prefix_pages, max_resp_pages); *bytes is a host pointer. */
+rp_status rp_group_decode_attn_workspace_size(const rp_paged_kv* kv,
+                                              const rp_group_layout* layout,
+                                              size_t* bytes);
+
+/* Group decode attention (the definition at the top of this file).
+ * q:   bf16 [num_seqs][num_q_heads][head_dim], 16-byte aligned.
+ * out: bf16 [num_seqs][num_q_heads][head_dim], 16-byte aligned.
+ * lse: fp32 [num_seqs][num_q_heads], natural log; may be NULL.
+ * softmax_scale: sigma, normally 1/sqrt(head_dim).
+ * workspace: device buffer of at least rp_group_decode_attn_workspace_size
+ *   bytes, 256-byte aligned, used for the work plan and partial results;
+ *   concurrent calls need distinct workspaces.
+ * Equivalent to rp_plan + rp_attn_parts + rp_combine_parts. */
+rp_status rp_group_decode_attn(const rp_paged_kv* kv, const rp_group_layout* layout,
+                               const void* q, float softmax_scale, void* out, float* lse,
+                               void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Log-sum-exp merge of partial attention results over disjoint key subsets.
+ * o_parts: fp32 [total_parts][head_dim], lse_parts: fp32 [total_parts] (natural
+ * log, -inf marks an empty part whose o is ignored); row r owns parts
+ * row_part_offsets[r] .. row_part_offsets[r+1]-1 (int32 CSR, [num_rows + 1]).
+ *   lse_out[r] = ln sum_i exp(lse_i),  out[r] = sum_i exp(lse_i - lse_out[r]) o_i
+ * out: bf16 [num_rows][head_dim]; lse_out: fp32 [num_rows] or NULL. A row with
+ * no non-empty part gets out = 0, lse = -inf. head_dim in {64, 128}. */
+rp_status rp_lse_combine(const float* o_parts, const float* lse_parts,
+                         const int32_t* row_part_offsets, int32_t num_rows, int32_t head_dim,
+                         void* out, float* lse_out, hipStream_t stream);
+
+/* ---- Staged form of rp_group_decode_attn -------------------------------
+ * A decode step's layout is shared by every layer, so a caller can plan once
+ * and run the attention of all layers against the same plan. */
+
+/* Build the work plan (group member lists, work items, CSR of partial results
+ * per (sequence, query head)) in `workspace` from the layout's device arrays.
+ * Must be re-run whenever seq_to_group, prefix_lens or resp_lens change. */
+rp_status rp_plan(const rp_paged_kv* kv, const rp_group_layout* layout,
+                  void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Compute all partial results for a planned workspace: the group-prefix parts
+ * (each group's prefix read once for all its members' query rows) and the
+ * response parts (split along each sequence's response pages). */
+rp_status rp_attn_parts(const rp_paged_kv* kv, const rp_group_layout* layout,
+                        const void* q, float softmax_scale,
+                        void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Merge the planned workspace's partial results into out / lse (same meaning
+ * as in rp_group_decode_attn); runs rp_lse_combine's kernel on them. */
+rp_status rp_combine_parts(const rp_paged_kv* kv, const rp_group_layout* layout,
+                           void* out, float* lse,
+                           void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Check the layout's device arrays against the pool and table sizes: groups
+ * in range, lengths non-negative and within the table widths, every page id
+ * that a length makes reachable in [0, num_pages). TEST UTILITY: allocates a
+ * small device buffer and synchronises `stream`. Returns RP_OK or
+ * RP_ERR_LAYOUT (detail in rp_last_error). */
+rp_status rp_validate_layout(const rp_paged_kv* kv, const rp_group_layout* layout,
+                             hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RP_H_ */

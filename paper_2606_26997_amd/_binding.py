@@ -1,0 +1,192 @@
+"""ctypes binding for librp.so: argument marshalling only.
+
+Every computation runs in the HIP library. torch is imported first so that the
+library's HIP runtime dependency resolves to the runtime torch already loaded;
+tensors are passed by ``data_ptr()`` and streams by their raw HIP handle.
+If the library is missing or cannot be loaded, every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch  # noqa: F401  (loads torch's HIP runtime before librp.so)
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "librp.so")
+
+RP_OK = 0
+RP_ERR_INVALID_ARG = 1
+RP_ERR_UNSUPPORTED = 2
+RP_ERR_WORKSPACE = 3
+RP_ERR_HIP = 4
+RP_ERR_LAYOUT = 5
+RP_KV_BF16 = 0
+RP_KV_FP8_E4M3 = 1
+
+EXPORTED = ("rp_status_string", "rp_last_error", "rp_kv_append",
+            "rp_group_decode_attn_workspace_size", "rp_group_decode_attn", "rp_lse_combine",
+            "rp_plan", "rp_attn_parts", "rp_combine_parts", "rp_validate_layout")
+
+
+class RpPagedKV(ctypes.Structure):
+    _fields_ = [("k_pages", ctypes.c_void_p), ("v_pages", ctypes.c_void_p),
+                ("k_scale", ctypes.c_void_p), ("v_scale", ctypes.c_void_p),
+                ("num_pages", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
+                ("page_size", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("kv_dtype", ctypes.c_int32)]
+
+
+class RpGroupLayout(ctypes.Structure):
+    _fields_ = [("num_seqs", ctypes.c_int32), ("num_groups", ctypes.c_int32),
+                ("num_q_heads", ctypes.c_int32),
+                ("seq_to_group", ctypes.c_void_p), ("prefix_lens", ctypes.c_void_p),
+                ("prefix_block_table", ctypes.c_void_p), ("max_prefix_pages", ctypes.c_int32),
+                ("resp_lens", ctypes.c_void_p), ("resp_block_table", ctypes.c_void_p),
+                ("max_resp_pages", ctypes.c_int32)]
+
+
+class RpError(RuntimeError):
+    def __init__(self, status: int, func: str, detail: str):
+        self.status = status
+        super().__init__(f"{func}: {status_string(status)}: {detail}")
+
+
+_lib = None
+
+
+def load() -> ctypes.CDLL:
+    """Load librp.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build()")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, I32, F32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_float
+    sig = {
+        "rp_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+        "rp_last_error": (ctypes.c_char_p, []),
+        "rp_kv_append": (ctypes.c_int, [P, P, P, P, P]),
+        "rp_group_decode_attn_workspace_size": (ctypes.c_int, [P, P, ctypes.POINTER(ctypes.c_size_t)]),
+        "rp_group_decode_attn": (ctypes.c_int, [P, P, P, F32, P, P, P, ctypes.c_size_t, P]),
+        "rp_lse_combine": (ctypes.c_int, [P, P, P, I32, I32, P, P, P]),
+        "rp_plan": (ctypes.c_int, [P, P, P, ctypes.c_size_t, P]),
+        "rp_attn_parts": (ctypes.c_int, [P, P, P, F32, P, ctypes.c_size_t, P]),
+        "rp_combine_parts": (ctypes.c_int, [P, P, P, P, P, ctypes.c_size_t, P]),
+        "rp_validate_layout": (ctypes.c_int, [P, P, P]),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(lib, name)
+        f.restype, f.argtypes = res, args
+    _lib = lib
+    return lib
+
+
+def status_string(status: int) -> str:
+    return load().rp_status_string(int(status)).decode()
+
+
+def last_error() -> str:
+    return load().rp_last_error().decode()
+
+
+def _check(status: int, func: str) -> None:
+    if status != RP_OK:
+        raise RpError(status, func, last_error())
+
+
+def _ptr(t) -> Optional[int]:
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream if torch.cuda.is_available() else None
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def paged_kv(k_pages, v_pages, k_scale=None, v_scale=None, *, num_pages=None, num_kv_heads=None,
+             page_size=16, head_dim=None, kv_dtype=None) -> RpPagedKV:
+    """Describe a pool of tensors shaped [num_pages][Hkv][page_size][head_dim]."""
+    shape = tuple(k_pages.shape) if hasattr(k_pages, "shape") else None
+    if kv_dtype is None:
+        kv_dtype = RP_KV_FP8_E4M3 if k_scale is not None else RP_KV_BF16
+    return RpPagedKV(_ptr(k_pages), _ptr(v_pages), _ptr(k_scale), _ptr(v_scale),
+                     num_pages if num_pages is not None else shape[0],
+                     num_kv_heads if num_kv_heads is not None else shape[1],
+                     page_size, head_dim if head_dim is not None else shape[3], kv_dtype)
+
+
+def group_layout(seq_to_group, prefix_lens, prefix_block_table, resp_lens, resp_block_table, *,
+                 num_q_heads, num_seqs=None, num_groups=None, max_prefix_pages=None,
+                 max_resp_pages=None) -> RpGroupLayout:
+    return RpGroupLayout(
+        num_seqs if num_seqs is not None else seq_to_group.shape[0],
+        num_groups if num_groups is not None else prefix_lens.shape[0],
+        num_q_heads, _ptr(seq_to_group), _ptr(prefix_lens), _ptr(prefix_block_table),
+        max_prefix_pages if max_prefix_pages is not None else prefix_block_table.shape[1],
+        _ptr(resp_lens), _ptr(resp_block_table),
+        max_resp_pages if max_resp_pages is not None else resp_block_table.shape[1])
+
+
+def kv_append(kv: RpPagedKV, layout: RpGroupLayout, k_new, v_new, stream=None) -> None:
+    _check(load().rp_kv_append(ctypes.byref(kv), ctypes.byref(layout), _ptr(k_new), _ptr(v_new),
+                               _stream(stream)), "rp_kv_append")
+
+
+def group_decode_attn_workspace_size(kv: RpPagedKV, layout: RpGroupLayout) -> int:
+    n = ctypes.c_size_t(0)
+    _check(load().rp_group_decode_attn_workspace_size(ctypes.byref(kv), ctypes.byref(layout),
+                                                      ctypes.byref(n)),
+           "rp_group_decode_attn_workspace_size")
+    return int(n.value)
+
+
+def _ws_bytes(workspace) -> int:
+    if workspace is None:
+        return 0
+    return workspace.numel() * workspace.element_size()
+
+
+def group_decode_attn(kv, layout, q, softmax_scale, out, lse, workspace, stream=None) -> None:
+    _check(load().rp_group_decode_attn(ctypes.byref(kv), ctypes.byref(layout), _ptr(q),
+                                       float(softmax_scale), _ptr(out), _ptr(lse), _ptr(workspace),
+                                       _ws_bytes(workspace), _stream(stream)),
+           "rp_group_decode_attn")
+
+
+def plan(kv, layout, workspace, stream=None) -> None:
+    _check(load().rp_plan(ctypes.byref(kv), ctypes.byref(layout), _ptr(workspace),
+                          _ws_bytes(workspace), _stream(stream)), "rp_plan")
+
+
+def attn_parts(kv, layout, q, softmax_scale, workspace, stream=None) -> None:
+    _check(load().rp_attn_parts(ctypes.byref(kv), ctypes.byref(layout), _ptr(q), float(softmax_scale),
+                                _ptr(workspace), _ws_bytes(workspace), _stream(stream)),
+           "rp_attn_parts")
+
+
+def combine_parts(kv, layout, out, lse, workspace, stream=None) -> None:
+    _check(load().rp_combine_parts(ctypes.byref(kv), ctypes.byref(layout), _ptr(out), _ptr(lse),
+                                   _ptr(workspace), _ws_bytes(workspace), _stream(stream)),
+           "rp_combine_parts")
+
+
+def lse_combine(o_parts, lse_parts, row_part_offsets, num_rows, head_dim, out, lse_out,
+                stream=None) -> None:
+    _check(load().rp_lse_combine(_ptr(o_parts), _ptr(lse_parts), _ptr(row_part_offsets),
+                                 int(num_rows), int(head_dim), _ptr(out), _ptr(lse_out),
+                                 _stream(stream)), "rp_lse_combine")
+
+
+def validate_layout(kv, layout, stream=None) -> None:
+    _check(load().rp_validate_layout(ctypes.byref(kv), ctypes.byref(layout), _stream(stream)),
+           "rp_validate_layout")

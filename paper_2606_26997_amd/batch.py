@@ -1,0 +1,109 @@
+"""Device-resident decode batch: torch tensors plus the C-ABI descriptors.
+
+Host arrays (numpy or torch) are copied to the device once; the descriptors
+point at those tensors. This is marshalling only: attention, append and
+combine all run in librp.so.
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from . import _binding as B
+
+
+def _dev(x, device, dtype=None):
+    if x is None:
+        return None
+    if isinstance(x, np.ndarray):
+        if x.dtype == np.uint16:
+            t = torch.from_numpy(x.view(np.int16)).view(torch.bfloat16)
+        elif x.dtype == np.uint8:
+            t = torch.from_numpy(x)
+        else:
+            t = torch.from_numpy(np.ascontiguousarray(x))
+    else:
+        t = x
+    if dtype is not None:
+        t = t.to(dtype)
+    return t.to(device).contiguous()
+
+
+class DeviceBatch:
+    """One decode step's inputs on the device.
+
+    ``resp_lens`` are the response tokens already cached. With ``append`` the
+    new token goes to slot ``resp_lens[s]`` and attention then reads
+    ``resp_lens + 1`` (the caller's length advance, done here once).
+    """
+
+    def __init__(self, *, k_pages, v_pages, k_scale, v_scale, seq_to_group, prefix_lens,
+                 prefix_block_table, resp_lens, resp_block_table, q, num_q_heads, softmax_scale,
+                 k_new=None, v_new=None, append=False, device="cuda"):
+        self.device = torch.device(device)
+        d = self.device
+        self.k_pages = _dev(k_pages, d)
+        self.v_pages = _dev(v_pages, d)
+        self.k_scale = _dev(k_scale, d, torch.float32)
+        self.v_scale = _dev(v_scale, d, torch.float32)
+        self.seq_to_group = _dev(seq_to_group, d, torch.int32)
+        self.prefix_lens = _dev(prefix_lens, d, torch.int32)
+        self.prefix_block_table = _dev(prefix_block_table, d, torch.int32)
+        self.resp_lens = _dev(resp_lens, d, torch.int32)
+        self.resp_block_table = _dev(resp_block_table, d, torch.int32)
+        self.q = _dev(q, d)
+        self.k_new = _dev(k_new, d)
+        self.v_new = _dev(v_new, d)
+        self.append = bool(append)
+        self.attn_resp_lens = self.resp_lens + 1 if self.append else self.resp_lens
+        self.num_q_heads = int(num_q_heads)
+        self.softmax_scale = float(softmax_scale)
+        S = self.seq_to_group.shape[0]
+        D = self.k_pages.shape[3]
+        self.out = torch.zeros((S, self.num_q_heads, D), dtype=torch.bfloat16, device=d)
+        self.lse = torch.zeros((S, self.num_q_heads), dtype=torch.float32, device=d)
+        self.kv = B.paged_kv(self.k_pages, self.v_pages, self.k_scale, self.v_scale)
+        self.append_layout = self._layout(self.resp_lens)
+        self.attn_layout = self._layout(self.attn_resp_lens)
+        ws = B.group_decode_attn_workspace_size(self.kv, self.attn_layout)
+        self.workspace = torch.empty(max(ws, 256), dtype=torch.uint8, device=d)
+
+    @classmethod
+    def from_workload(cls, wl, device="cuda"):
+        return cls(k_pages=wl.k_pages, v_pages=wl.v_pages, k_scale=wl.k_scale, v_scale=wl.v_scale,
+                   seq_to_group=wl.seq_to_group, prefix_lens=wl.prefix_lens,
+                   prefix_block_table=wl.prefix_block_table, resp_lens=wl.resp_lens,
+                   resp_block_table=wl.resp_block_table, q=wl.q, num_q_heads=wl.num_q_heads,
+                   softmax_scale=wl.softmax_scale, k_new=wl.k_new, v_new=wl.v_new,
+                   append=wl.append, device=device)
+
+    def _layout(self, resp_lens):
+        return B.group_layout(self.seq_to_group, self.prefix_lens, self.prefix_block_table, resp_lens,
+                              self.resp_block_table, num_q_heads=self.num_q_heads)
+
+    # -- the decode step ------------------------------------------------------
+    def kv_append(self, stream=None):
+        B.kv_append(self.kv, self.append_layout, self.k_new, self.v_new, stream)
+
+    def attention(self, stream=None):
+        B.group_decode_attn(self.kv, self.attn_layout, self.q, self.softmax_scale, self.out, self.lse,
+                            self.workspace, stream)
+
+    def step(self, stream=None):
+        """Append (if the batch carries new tokens) and attention."""
+        if self.append:
+            self.kv_append(stream)
+        self.attention(stream)
+
+    # -- staged form ------------------------------------------------------------
+    def plan(self, stream=None):
+        B.plan(self.kv, self.attn_layout, self.workspace, stream)
+
+    def attn_parts(self, stream=None):
+        B.attn_parts(self.kv, self.attn_layout, self.q, self.softmax_scale, self.workspace, stream)
+
+    def combine_parts(self, stream=None):
+        B.combine_parts(self.kv, self.attn_layout, self.out, self.lse, self.workspace, stream)
+
+    def validate(self, stream=None):
+        B.validate_layout(self.kv, self.attn_layout, stream)

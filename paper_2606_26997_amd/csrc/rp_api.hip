@@ -1,0 +1,388 @@
+// C-ABI entry points: argument validation, workspace layout and kernel
+// launches on the caller's stream. No device allocation and no host sync on
+// the hot path; rp_validate_layout is the one test utility that does both.
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+#include "rp.h"
+#include "rp_internal.h"
+
+namespace {
+
+thread_local char g_err[512];
+
+rp_status fail(rp_status st, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return st;
+}
+
+rp_status hip_fail(hipError_t e, const char* what) {
+  return fail(RP_ERR_HIP, "%s: %s (%d)", what, hipGetErrorString(e), (int)e);
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+struct Shape {
+  int S, G, Hq, Hkv, D, nrep, max_pp, max_rp, num_pages;
+  bool fp8;
+};
+
+rp_status check_kv(const rp_paged_kv* kv) {
+  if (kv == nullptr) return fail(RP_ERR_INVALID_ARG, "kv is NULL");
+  if (kv->k_pages == nullptr || kv->v_pages == nullptr) return fail(RP_ERR_INVALID_ARG, "k_pages/v_pages is NULL");
+  if (!aligned(kv->k_pages, 16) || !aligned(kv->v_pages, 16))
+    return fail(RP_ERR_INVALID_ARG, "k_pages/v_pages must be 16-byte aligned");
+  if (kv->num_pages < 1) return fail(RP_ERR_INVALID_ARG, "num_pages must be >= 1 (got %d)", kv->num_pages);
+  if (kv->num_kv_heads < 1) return fail(RP_ERR_INVALID_ARG, "num_kv_heads must be >= 1");
+  if (kv->page_size != rp::kPage) return fail(RP_ERR_UNSUPPORTED, "page_size %d unsupported (16 only)", kv->page_size);
+  if (kv->head_dim != 64 && kv->head_dim != 128)
+    return fail(RP_ERR_UNSUPPORTED, "head_dim %d unsupported (64 or 128)", kv->head_dim);
+  if (kv->kv_dtype == RP_KV_BF16) {
+    if (kv->k_scale != nullptr || kv->v_scale != nullptr)
+      return fail(RP_ERR_INVALID_ARG, "k_scale/v_scale must be NULL for bf16 KV");
+  } else if (kv->kv_dtype == RP_KV_FP8_E4M3) {
+    if (kv->k_scale == nullptr || kv->v_scale == nullptr)
+      return fail(RP_ERR_INVALID_ARG, "k_scale/v_scale required for fp8 KV");
+    if (!aligned(kv->k_scale, 4) || !aligned(kv->v_scale, 4))
+      return fail(RP_ERR_INVALID_ARG, "k_scale/v_scale must be 4-byte aligned");
+  } else {
+    return fail(RP_ERR_UNSUPPORTED, "kv_dtype %d unsupported", (int)kv->kv_dtype);
+  }
+  return RP_OK;
+}
+
+rp_status check_shape(const rp_paged_kv* kv, const rp_group_layout* l, Shape* sh) {
+  rp_status st = check_kv(kv);
+  if (st != RP_OK) return st;
+  if (l == nullptr) return fail(RP_ERR_INVALID_ARG, "layout is NULL");
+  if (l->num_seqs < 0) return fail(RP_ERR_INVALID_ARG, "num_seqs must be >= 0");
+  if (l->num_q_heads < 1) return fail(RP_ERR_INVALID_ARG, "num_q_heads must be >= 1");
+  if (l->num_q_heads % kv->num_kv_heads != 0)
+    return fail(RP_ERR_INVALID_ARG, "num_q_heads %d not a multiple of num_kv_heads %d", l->num_q_heads,
+                kv->num_kv_heads);
+  const int nrep = l->num_q_heads / kv->num_kv_heads;
+  if (nrep != 1 && nrep != 2 && nrep != 4 && nrep != 8)
+    return fail(RP_ERR_UNSUPPORTED, "q/kv head ratio %d unsupported (1, 2, 4, 8)", nrep);
+  if (l->max_prefix_pages < 0 || l->max_resp_pages < 0)
+    return fail(RP_ERR_INVALID_ARG, "table widths must be >= 0");
+  if (l->num_seqs > 0) {
+    if (l->num_groups < 1) return fail(RP_ERR_INVALID_ARG, "num_groups must be >= 1");
+    if (l->seq_to_group == nullptr || l->prefix_lens == nullptr || l->resp_lens == nullptr)
+      return fail(RP_ERR_INVALID_ARG, "seq_to_group/prefix_lens/resp_lens is NULL");
+    if (l->max_prefix_pages > 0 && l->prefix_block_table == nullptr)
+      return fail(RP_ERR_INVALID_ARG, "prefix_block_table is NULL");
+    if (l->max_resp_pages > 0 && l->resp_block_table == nullptr)
+      return fail(RP_ERR_INVALID_ARG, "resp_block_table is NULL");
+  }
+  // Every index the kernels form stays below 2^31 elements per int32 table.
+  const long long rows = (long long)l->num_seqs * l->num_q_heads;
+  if ((long long)l->num_seqs * l->max_resp_pages >= (1ll << 31) ||
+      (long long)l->num_groups * l->max_prefix_pages >= (1ll << 31) || rows >= (1ll << 31))
+    return fail(RP_ERR_UNSUPPORTED, "layout too large for int32 indexing");
+  sh->S = l->num_seqs;
+  sh->G = l->num_groups;
+  sh->Hq = l->num_q_heads;
+  sh->Hkv = kv->num_kv_heads;
+  sh->D = kv->head_dim;
+  sh->nrep = nrep;
+  sh->max_pp = l->max_prefix_pages;
+  sh->max_rp = l->max_resp_pages;
+  sh->num_pages = kv->num_pages;
+  sh->fp8 = kv->kv_dtype == RP_KV_FP8_E4M3;
+  return RP_OK;
+}
+
+// Workspace layout, 256-byte aligned sections.
+struct WsLayout {
+  size_t hdr, grp_count, grp_fill, grp_off, members, pitems, ritems, row_offs, part_o, part_lse, total;
+  long long max_pitems, max_ritems, max_parts;
+  int max_pc, max_rc;
+};
+
+size_t align_up(size_t x) { return (x + 255) & ~size_t(255); }
+
+bool ws_layout(const Shape& sh, WsLayout* w) {
+  w->max_pc = rp::cdiv(sh.max_pp, rp::kPrefixChunkPages);
+  w->max_rc = rp::cdiv(sh.max_rp, rp::kRespChunkPages);
+  const long long groups_used = sh.G < sh.S ? sh.G : sh.S;
+  w->max_pitems = groups_used * w->max_pc;
+  w->max_ritems = (long long)sh.S * w->max_rc;
+  w->max_parts = (long long)sh.S * sh.Hq * (w->max_pc + w->max_rc);
+  if (w->max_parts >= (1ll << 31) || w->max_ritems * sh.Hkv >= (1ll << 31) ||
+      w->max_pitems * sh.Hkv >= (1ll << 31))
+    return false;
+  size_t o = 0;
+  w->hdr = o;       o = align_up(o + sizeof(int) * rp::kHdrSlots);
+  w->grp_count = o; o = align_up(o + sizeof(int) * (size_t)sh.G);
+  w->grp_fill = o;  o = align_up(o + sizeof(int) * (size_t)sh.G);
+  w->grp_off = o;   o = align_up(o + sizeof(int) * ((size_t)sh.G + 1));
+  w->members = o;   o = align_up(o + sizeof(int) * (size_t)sh.S);
+  w->pitems = o;    o = align_up(o + sizeof(int2) * (size_t)w->max_pitems);
+  w->ritems = o;    o = align_up(o + sizeof(int2) * (size_t)w->max_ritems);
+  w->row_offs = o;  o = align_up(o + sizeof(int) * ((size_t)sh.S * sh.Hq + 1));
+  w->part_o = o;    o = align_up(o + sizeof(float) * (size_t)w->max_parts * sh.D);
+  w->part_lse = o;  o = align_up(o + sizeof(float) * (size_t)w->max_parts);
+  w->total = o;
+  return true;
+}
+
+rp::PlanView plan_view(void* ws, const WsLayout& w) {
+  char* b = static_cast<char*>(ws);
+  rp::PlanView v;
+  v.hdr = reinterpret_cast<int*>(b + w.hdr);
+  v.grp_count = reinterpret_cast<int*>(b + w.grp_count);
+  v.grp_fill = reinterpret_cast<int*>(b + w.grp_fill);
+  v.grp_off = reinterpret_cast<int*>(b + w.grp_off);
+  v.grp_members = reinterpret_cast<int*>(b + w.members);
+  v.prefix_items = reinterpret_cast<int2*>(b + w.pitems);
+  v.resp_items = reinterpret_cast<int2*>(b + w.ritems);
+  v.row_offs = reinterpret_cast<int*>(b + w.row_offs);
+  v.part_o = reinterpret_cast<float*>(b + w.part_o);
+  v.part_lse = reinterpret_cast<float*>(b + w.part_lse);
+  v.max_prefix_chunks = w.max_pc;
+  v.max_resp_chunks = w.max_rc;
+  v.max_parts = (int)w.max_parts;
+  return v;
+}
+
+rp_status prepare(const rp_paged_kv* kv, const rp_group_layout* l, void* ws, size_t ws_bytes, Shape* sh,
+                  WsLayout* w) {
+  rp_status st = check_shape(kv, l, sh);
+  if (st != RP_OK) return st;
+  if (!ws_layout(*sh, w)) return fail(RP_ERR_UNSUPPORTED, "layout too large for the work plan");
+  if (sh->S == 0) return RP_OK;
+  if (ws == nullptr) return fail(RP_ERR_WORKSPACE, "workspace is NULL");
+  if (!aligned(ws, 256)) return fail(RP_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  if (ws_bytes < w->total)
+    return fail(RP_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, w->total);
+  return RP_OK;
+}
+
+rp::AttnArgs attn_args(const rp_paged_kv* kv, const rp_group_layout* l, const void* q, float scale,
+                       const rp::PlanView& v) {
+  rp::AttnArgs a;
+  a.k_pages = kv->k_pages;
+  a.v_pages = kv->v_pages;
+  a.k_scale = kv->k_scale;
+  a.v_scale = kv->v_scale;
+  a.num_pages = kv->num_pages;
+  a.num_kv_heads = kv->num_kv_heads;
+  a.num_seqs = l->num_seqs;
+  a.num_groups = l->num_groups;
+  a.num_q_heads = l->num_q_heads;
+  a.seq_to_group = l->seq_to_group;
+  a.prefix_lens = l->prefix_lens;
+  a.prefix_block_table = l->prefix_block_table;
+  a.max_prefix_pages = l->max_prefix_pages;
+  a.resp_lens = l->resp_lens;
+  a.resp_block_table = l->resp_block_table;
+  a.max_resp_pages = l->max_resp_pages;
+  a.q = q;
+  a.qk_scale = scale * rp::kLog2e;
+  a.view = v;
+  return a;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* rp_status_string(rp_status status) {
+  switch (status) {
+    case RP_OK: return "RP_OK: success";
+    case RP_ERR_INVALID_ARG: return "RP_ERR_INVALID_ARG: invalid argument";
+    case RP_ERR_UNSUPPORTED: return "RP_ERR_UNSUPPORTED: unsupported configuration";
+    case RP_ERR_WORKSPACE: return "RP_ERR_WORKSPACE: workspace missing or too small";
+    case RP_ERR_HIP: return "RP_ERR_HIP: HIP runtime error";
+    case RP_ERR_LAYOUT: return "RP_ERR_LAYOUT: layout entry out of range";
+  }
+  return "unknown rp_status";
+}
+
+const char* rp_last_error(void) { return g_err; }
+
+rp_status rp_group_decode_attn_workspace_size(const rp_paged_kv* kv, const rp_group_layout* layout,
+                                              size_t* bytes) {
+  g_err[0] = 0;
+  if (bytes == nullptr) return fail(RP_ERR_INVALID_ARG, "bytes is NULL");
+  Shape sh;
+  rp_status st = check_shape(kv, layout, &sh);
+  if (st != RP_OK) return st;
+  WsLayout w;
+  if (!ws_layout(sh, &w)) return fail(RP_ERR_UNSUPPORTED, "layout too large for the work plan");
+  *bytes = sh.S == 0 ? 0 : w.total;
+  return RP_OK;
+}
+
+rp_status rp_plan(const rp_paged_kv* kv, const rp_group_layout* l, void* ws, size_t ws_bytes,
+                  hipStream_t stream) {
+  g_err[0] = 0;
+  Shape sh;
+  WsLayout w;
+  rp_status st = prepare(kv, l, ws, ws_bytes, &sh, &w);
+  if (st != RP_OK || sh.S == 0) return st;
+  rp::PlanArgs a;
+  a.num_seqs = sh.S;
+  a.num_groups = sh.G;
+  a.num_q_heads = sh.Hq;
+  a.seq_to_group = l->seq_to_group;
+  a.prefix_lens = l->prefix_lens;
+  a.resp_lens = l->resp_lens;
+  a.max_prefix_pages = sh.max_pp;
+  a.max_resp_pages = sh.max_rp;
+  a.view = plan_view(ws, w);
+  hipError_t e = rp::launch_plan(a, stream);
+  return e == hipSuccess ? RP_OK : hip_fail(e, "plan kernel launch");
+}
+
+rp_status rp_attn_parts(const rp_paged_kv* kv, const rp_group_layout* l, const void* q, float softmax_scale,
+                        void* ws, size_t ws_bytes, hipStream_t stream) {
+  g_err[0] = 0;
+  Shape sh;
+  WsLayout w;
+  rp_status st = prepare(kv, l, ws, ws_bytes, &sh, &w);
+  if (st != RP_OK || sh.S == 0) return st;
+  if (q == nullptr || !aligned(q, 16)) return fail(RP_ERR_INVALID_ARG, "q must be non-NULL and 16-byte aligned");
+  const rp::AttnArgs a = attn_args(kv, l, q, softmax_scale, plan_view(ws, w));
+  hipError_t e = rp::launch_prefix_parts(a, sh.D, sh.nrep, sh.fp8, w.max_pitems, stream);
+  if (e != hipSuccess) return hip_fail(e, "prefix kernel launch");
+  e = rp::launch_resp_parts(a, sh.D, sh.nrep, sh.fp8, w.max_ritems, stream);
+  if (e != hipSuccess) return hip_fail(e, "response kernel launch");
+  return RP_OK;
+}
+
+rp_status rp_combine_parts(const rp_paged_kv* kv, const rp_group_layout* l, void* out, float* lse, void* ws,
+                           size_t ws_bytes, hipStream_t stream) {
+  g_err[0] = 0;
+  Shape sh;
+  WsLayout w;
+  rp_status st = prepare(kv, l, ws, ws_bytes, &sh, &w);
+  if (st != RP_OK || sh.S == 0) return st;
+  if (out == nullptr || !aligned(out, 16)) return fail(RP_ERR_INVALID_ARG, "out must be non-NULL and 16-byte aligned");
+  if (lse != nullptr && !aligned(lse, 4)) return fail(RP_ERR_INVALID_ARG, "lse must be 4-byte aligned");
+  const rp::PlanView v = plan_view(ws, w);
+  rp::CombineArgs c;
+  c.o_parts = v.part_o;
+  c.lse_parts = v.part_lse;
+  c.row_offs = v.row_offs;
+  c.num_rows = sh.S * sh.Hq;
+  c.out = out;
+  c.lse = lse;
+  hipError_t e = rp::launch_combine(c, sh.D, stream);
+  return e == hipSuccess ? RP_OK : hip_fail(e, "combine kernel launch");
+}
+
+rp_status rp_group_decode_attn(const rp_paged_kv* kv, const rp_group_layout* l, const void* q,
+                               float softmax_scale, void* out, float* lse, void* ws, size_t ws_bytes,
+                               hipStream_t stream) {
+  g_err[0] = 0;
+  Shape sh;
+  WsLayout w;
+  rp_status st = prepare(kv, l, ws, ws_bytes, &sh, &w);
+  if (st != RP_OK || sh.S == 0) return st;
+  if (q == nullptr || !aligned(q, 16)) return fail(RP_ERR_INVALID_ARG, "q must be non-NULL and 16-byte aligned");
+  if (out == nullptr || !aligned(out, 16)) return fail(RP_ERR_INVALID_ARG, "out must be non-NULL and 16-byte aligned");
+  if (lse != nullptr && !aligned(lse, 4)) return fail(RP_ERR_INVALID_ARG, "lse must be 4-byte aligned");
+  st = rp_plan(kv, l, ws, ws_bytes, stream);
+  if (st != RP_OK) return st;
+  st = rp_attn_parts(kv, l, q, softmax_scale, ws, ws_bytes, stream);
+  if (st != RP_OK) return st;
+  return rp_combine_parts(kv, l, out, lse, ws, ws_bytes, stream);
+}
+
+rp_status rp_lse_combine(const float* o_parts, const float* lse_parts, const int32_t* row_part_offsets,
+                         int32_t num_rows, int32_t head_dim, void* out, float* lse_out, hipStream_t stream) {
+  g_err[0] = 0;
+  if (num_rows < 0) return fail(RP_ERR_INVALID_ARG, "num_rows must be >= 0");
+  if (head_dim != 64 && head_dim != 128) return fail(RP_ERR_UNSUPPORTED, "head_dim %d unsupported", head_dim);
+  if (num_rows == 0) return RP_OK;
+  if (row_part_offsets == nullptr || out == nullptr)
+    return fail(RP_ERR_INVALID_ARG, "row_part_offsets/out is NULL");
+  if (!aligned(out, 4)) return fail(RP_ERR_INVALID_ARG, "out must be 4-byte aligned");
+  if (lse_out != nullptr && !aligned(lse_out, 4)) return fail(RP_ERR_INVALID_ARG, "lse_out must be 4-byte aligned");
+  if ((o_parts != nullptr && !aligned(o_parts, 8)) || (lse_parts != nullptr && !aligned(lse_parts, 4)))
+    return fail(RP_ERR_INVALID_ARG, "o_parts must be 8-byte and lse_parts 4-byte aligned");
+  rp::CombineArgs c;
+  c.o_parts = o_parts;
+  c.lse_parts = lse_parts;
+  c.row_offs = row_part_offsets;
+  c.num_rows = num_rows;
+  c.out = out;
+  c.lse = lse_out;
+  hipError_t e = rp::launch_combine(c, head_dim, stream);
+  return e == hipSuccess ? RP_OK : hip_fail(e, "combine kernel launch");
+}
+
+rp_status rp_kv_append(const rp_paged_kv* kv, const rp_group_layout* l, const void* k_new, const void* v_new,
+                       hipStream_t stream) {
+  g_err[0] = 0;
+  Shape sh;
+  rp_status st = check_shape(kv, l, &sh);
+  if (st != RP_OK) return st;
+  if (sh.S == 0) return RP_OK;
+  if (k_new == nullptr || v_new == nullptr || !aligned(k_new, 16) || !aligned(v_new, 16))
+    return fail(RP_ERR_INVALID_ARG, "k_new/v_new must be non-NULL and 16-byte aligned");
+  if (sh.max_rp < 1) return fail(RP_ERR_INVALID_ARG, "max_resp_pages must be >= 1 to append");
+  rp::AppendArgs a;
+  a.k_pages = kv->k_pages;
+  a.v_pages = kv->v_pages;
+  a.k_scale = kv->k_scale;
+  a.v_scale = kv->v_scale;
+  a.num_pages = kv->num_pages;
+  a.num_kv_heads = kv->num_kv_heads;
+  a.num_seqs = sh.S;
+  a.resp_lens = l->resp_lens;
+  a.resp_block_table = l->resp_block_table;
+  a.max_resp_pages = sh.max_rp;
+  a.k_new = k_new;
+  a.v_new = v_new;
+  hipError_t e = rp::launch_append(a, sh.D, sh.fp8, stream);
+  return e == hipSuccess ? RP_OK : hip_fail(e, "append kernel launch");
+}
+
+rp_status rp_validate_layout(const rp_paged_kv* kv, const rp_group_layout* l, hipStream_t stream) {
+  g_err[0] = 0;
+  Shape sh;
+  rp_status st = check_shape(kv, l, &sh);
+  if (st != RP_OK) return st;
+  if (sh.S == 0) return RP_OK;
+  int* dres = nullptr;
+  hipError_t e = hipMalloc(&dres, 4 * sizeof(int));
+  if (e != hipSuccess) return hip_fail(e, "hipMalloc");
+  int hres[4] = {0, 0, 0, 0};
+  e = hipMemcpyAsync(dres, hres, sizeof(hres), hipMemcpyHostToDevice, stream);
+  if (e == hipSuccess) {
+    rp::ValidateArgs a;
+    a.num_pages = sh.num_pages;
+    a.num_seqs = sh.S;
+    a.num_groups = sh.G;
+    a.seq_to_group = l->seq_to_group;
+    a.prefix_lens = l->prefix_lens;
+    a.prefix_block_table = l->prefix_block_table;
+    a.max_prefix_pages = sh.max_pp;
+    a.resp_lens = l->resp_lens;
+    a.resp_block_table = l->resp_block_table;
+    a.max_resp_pages = sh.max_rp;
+    a.result = dres;
+    e = rp::launch_validate(a, stream);
+  }
+  if (e == hipSuccess) e = hipMemcpyAsync(hres, dres, sizeof(hres), hipMemcpyDeviceToHost, stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(stream);
+  hipError_t ef = hipFree(dres);
+  if (e != hipSuccess) return hip_fail(e, "validate_layout");
+  if (ef != hipSuccess) return hip_fail(ef, "hipFree");
+  if (hres[0] != 0) {
+    static const char* kinds[] = {"?", "seq_to_group", "prefix_lens", "resp_lens", "prefix_block_table",
+                                  "resp_block_table"};
+    const int k = (hres[1] >= 1 && hres[1] <= 5) ? hres[1] : 0;
+    return fail(RP_ERR_LAYOUT, "%d bad entries; e.g. %s at index %d has value %d", hres[0], kinds[k], hres[2],
+                hres[3]);
+  }
+  return RP_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,102 @@
+// Host/device interface between the C-ABI layer and the kernel launchers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "rp_device.h"
+
+namespace rp {
+
+// Lengths and group ids are clamped into the table/pool bounds before use, so
+// an invalid layout gives wrong numbers but never an out-of-bounds access.
+__host__ __device__ inline int clamp_group(int g, int G) { return g < 0 ? 0 : (g >= G ? G - 1 : g); }
+__host__ __device__ inline int clamp_len(int len, int max_pages) {
+  const int cap = max_pages * kPage;
+  return len < 0 ? 0 : (len > cap ? cap : len);
+}
+__host__ __device__ inline int prefix_chunks(int P, int max_prefix_pages, int max_chunks) {
+  const int n = cdiv(cdiv(clamp_len(P, max_prefix_pages), kPage), kPrefixChunkPages);
+  return n > max_chunks ? max_chunks : n;
+}
+__host__ __device__ inline int resp_chunks(int L, int max_resp_pages, int max_chunks) {
+  const int n = cdiv(cdiv(clamp_len(L, max_resp_pages), kPage), kRespChunkPages);
+  return n > max_chunks ? max_chunks : n;
+}
+__device__ inline int clamp_page(int p, int num_pages) {
+  return (unsigned)p < (unsigned)num_pages ? p : 0;
+}
+
+struct PlanArgs {
+  int num_seqs, num_groups, num_q_heads;
+  const int* seq_to_group;
+  const int* prefix_lens;
+  const int* resp_lens;
+  int max_prefix_pages, max_resp_pages;
+  PlanView view;
+};
+
+struct AttnArgs {
+  const void* k_pages;
+  const void* v_pages;
+  const float* k_scale;
+  const float* v_scale;
+  int num_pages, num_kv_heads;
+  int num_seqs, num_groups, num_q_heads;
+  const int* seq_to_group;
+  const int* prefix_lens;
+  const int* prefix_block_table;
+  int max_prefix_pages;
+  const int* resp_lens;
+  const int* resp_block_table;
+  int max_resp_pages;
+  const void* q;     // bf16 [S][Hq][D]
+  float qk_scale;    // softmax_scale * log2(e)
+  PlanView view;
+};
+
+struct CombineArgs {
+  const float* o_parts;
+  const float* lse_parts;
+  const int* row_offs;
+  int num_rows;
+  void* out;         // bf16 [rows][D]
+  float* lse;        // [rows] or null
+};
+
+struct AppendArgs {
+  void* k_pages;
+  void* v_pages;
+  float* k_scale;
+  float* v_scale;
+  int num_pages, num_kv_heads, num_seqs;
+  const int* resp_lens;
+  const int* resp_block_table;
+  int max_resp_pages;
+  const void* k_new;  // bf16 [S][Hkv][D]
+  const void* v_new;
+};
+
+struct ValidateArgs {
+  int num_pages, num_seqs, num_groups;
+  const int* seq_to_group;
+  const int* prefix_lens;
+  const int* prefix_block_table;
+  int max_prefix_pages;
+  const int* resp_lens;
+  const int* resp_block_table;
+  int max_resp_pages;
+  int* result;       // [4]: error count, first bad kind, first bad index, value
+};
+
+hipError_t launch_plan(const PlanArgs& a, hipStream_t stream);
+// grid sizes are upper bounds from host scalars; idle waves exit at once.
+hipError_t launch_prefix_parts(const AttnArgs& a, int head_dim, int n_rep, bool fp8,
+                               long long max_items, hipStream_t stream);
+hipError_t launch_resp_parts(const AttnArgs& a, int head_dim, int n_rep, bool fp8,
+                             long long max_items, hipStream_t stream);
+hipError_t launch_combine(const CombineArgs& a, int head_dim, hipStream_t stream);
+hipError_t launch_append(const AppendArgs& a, int head_dim, bool fp8, hipStream_t stream);
+hipError_t launch_validate(const ValidateArgs& a, hipStream_t stream);
+
+}  // namespace rp

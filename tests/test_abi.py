@@ -1,0 +1,152 @@
+"""C-ABI checks that need no GPU: exported symbols and synchronous argument validation.
+
+Every call here fails validation before anything reaches the HIP runtime.
+"""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+import paper_2606_26997_amd as rp
+from paper_2606_26997_amd import _binding as B
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "rp.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(rp_\w+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function():
+    names = declared_functions()
+    assert len(names) >= 10
+    out = subprocess.run(["nm", "-D", "--defined-only", B.LIB_PATH], capture_output=True, text=True,
+                         check=True).stdout
+    exported = set(re.findall(r"\bT (rp_\w+)", out))
+    assert set(names) <= exported, set(names) - exported
+    assert set(names) == set(B.EXPORTED)
+    lib = rp.load()
+    for n in names:
+        assert getattr(lib, n) is not None
+
+
+def test_status_strings():
+    for code, tag in [(0, "RP_OK"), (1, "INVALID_ARG"), (2, "UNSUPPORTED"), (3, "WORKSPACE"),
+                      (4, "HIP"), (5, "LAYOUT")]:
+        assert tag in rp.status_string(code)
+    assert "unknown" in rp.status_string(99)
+
+
+# Fake but 256-aligned "device" addresses: validation never dereferences them.
+A = 0x10000000
+
+
+def _kv(**kw):
+    d = dict(k_pages=A, v_pages=A + 4096, k_scale=None, v_scale=None, num_pages=4, num_kv_heads=2,
+             page_size=16, head_dim=64, kv_dtype=rp.RP_KV_BF16)
+    d.update(kw)
+    return B.RpPagedKV(d["k_pages"], d["v_pages"], d["k_scale"], d["v_scale"], d["num_pages"],
+                       d["num_kv_heads"], d["page_size"], d["head_dim"], d["kv_dtype"])
+
+
+def _layout(**kw):
+    d = dict(num_seqs=2, num_groups=1, num_q_heads=4, seq_to_group=A, prefix_lens=A, pbt=A, mpp=2,
+             resp_lens=A, rbt=A, mrp=2)
+    d.update(kw)
+    return B.RpGroupLayout(d["num_seqs"], d["num_groups"], d["num_q_heads"], d["seq_to_group"],
+                           d["prefix_lens"], d["pbt"], d["mpp"], d["resp_lens"], d["rbt"], d["mrp"])
+
+
+def _ws_size(kv, layout):
+    n = ctypes.c_size_t(0)
+    st = rp.load().rp_group_decode_attn_workspace_size(ctypes.byref(kv) if kv is not None else None,
+                                                       ctypes.byref(layout) if layout is not None else None,
+                                                       ctypes.byref(n))
+    return st, n.value
+
+
+@pytest.mark.parametrize("kv_kw,lay_kw,status,needle", [
+    (dict(k_pages=None), {}, rp.RP_ERR_INVALID_ARG, "NULL"),
+    (dict(k_pages=A + 8), {}, rp.RP_ERR_INVALID_ARG, "aligned"),
+    (dict(page_size=32), {}, rp.RP_ERR_UNSUPPORTED, "page_size"),
+    (dict(head_dim=96), {}, rp.RP_ERR_UNSUPPORTED, "head_dim"),
+    (dict(kv_dtype=rp.RP_KV_FP8_E4M3), {}, rp.RP_ERR_INVALID_ARG, "scale"),
+    (dict(k_scale=A), {}, rp.RP_ERR_INVALID_ARG, "NULL for bf16"),
+    (dict(kv_dtype=7), {}, rp.RP_ERR_UNSUPPORTED, "kv_dtype"),
+    (dict(num_pages=0), {}, rp.RP_ERR_INVALID_ARG, "num_pages"),
+    ({}, dict(num_q_heads=3), rp.RP_ERR_INVALID_ARG, "multiple"),
+    ({}, dict(num_q_heads=6), rp.RP_ERR_UNSUPPORTED, "ratio"),
+    ({}, dict(num_groups=0), rp.RP_ERR_INVALID_ARG, "num_groups"),
+    ({}, dict(seq_to_group=None), rp.RP_ERR_INVALID_ARG, "NULL"),
+    ({}, dict(rbt=None), rp.RP_ERR_INVALID_ARG, "resp_block_table"),
+    ({}, dict(num_seqs=-1), rp.RP_ERR_INVALID_ARG, "num_seqs"),
+])
+def test_invalid_arguments_rejected(kv_kw, lay_kw, status, needle):
+    st, _ = _ws_size(_kv(**kv_kw), _layout(**lay_kw))
+    assert st == status
+    assert needle in rp.last_error()
+
+
+def test_null_structs_rejected():
+    assert _ws_size(None, _layout())[0] == rp.RP_ERR_INVALID_ARG
+    assert _ws_size(_kv(), None)[0] == rp.RP_ERR_INVALID_ARG
+
+
+def test_workspace_size_depends_only_on_scalars_and_grows():
+    st, n1 = _ws_size(_kv(), _layout(mrp=2))
+    st2, n2 = _ws_size(_kv(), _layout(mrp=200))
+    assert st == st2 == rp.RP_OK and 0 < n1 < n2
+    assert _ws_size(_kv(), _layout(num_seqs=0))[1] == 0
+
+
+def test_short_or_misaligned_workspace_rejected():
+    kv, lay = _kv(), _layout()
+    _, need = _ws_size(kv, lay)
+    lib = rp.load()
+    st = lib.rp_plan(ctypes.byref(kv), ctypes.byref(lay), A, need - 1, None)
+    assert st == rp.RP_ERR_WORKSPACE and "needs" in rp.last_error()
+    st = lib.rp_plan(ctypes.byref(kv), ctypes.byref(lay), A + 64, need, None)
+    assert st == rp.RP_ERR_WORKSPACE and "aligned" in rp.last_error()
+    st = lib.rp_group_decode_attn(ctypes.byref(kv), ctypes.byref(lay), A, ctypes.c_float(0.1), A, None,
+                                  None, need, None)
+    assert st == rp.RP_ERR_WORKSPACE
+
+
+def test_attention_and_append_pointer_checks():
+    kv, lay = _kv(), _layout()
+    _, need = _ws_size(kv, lay)
+    lib = rp.load()
+    st = lib.rp_group_decode_attn(ctypes.byref(kv), ctypes.byref(lay), None, ctypes.c_float(0.1), A, None,
+                                  A, need, None)
+    assert st == rp.RP_ERR_INVALID_ARG and "q" in rp.last_error()
+    st = lib.rp_group_decode_attn(ctypes.byref(kv), ctypes.byref(lay), A, ctypes.c_float(0.1), A + 2, None,
+                                  A, need, None)
+    assert st == rp.RP_ERR_INVALID_ARG and "out" in rp.last_error()
+    assert lib.rp_kv_append(ctypes.byref(kv), ctypes.byref(lay), None, A, None) == rp.RP_ERR_INVALID_ARG
+    assert lib.rp_kv_append(ctypes.byref(kv), ctypes.byref(_layout(mrp=0)), A, A, None) == rp.RP_ERR_INVALID_ARG
+
+
+def test_lse_combine_argument_checks():
+    lib = rp.load()
+    assert lib.rp_lse_combine(A, A, A, 4, 96, A, None, None) == rp.RP_ERR_UNSUPPORTED
+    assert lib.rp_lse_combine(A, A, None, 4, 128, A, None, None) == rp.RP_ERR_INVALID_ARG
+    assert lib.rp_lse_combine(A, A, A, -1, 128, A, None, None) == rp.RP_ERR_INVALID_ARG
+    assert lib.rp_lse_combine(None, None, None, 0, 128, None, None, None) == rp.RP_OK
+
+
+def test_empty_batch_is_a_no_op():
+    kv, lay = _kv(), _layout(num_seqs=0)
+    lib = rp.load()
+    assert lib.rp_group_decode_attn(ctypes.byref(kv), ctypes.byref(lay), None, ctypes.c_float(0.1), None,
+                                    None, None, 0, None) == rp.RP_OK
+    assert lib.rp_kv_append(ctypes.byref(kv), ctypes.byref(lay), None, None, None) == rp.RP_OK
+
+
+def test_binding_raises_with_detail():
+    with pytest.raises(rp.RpError) as e:
+        B._check(rp.RP_ERR_UNSUPPORTED, "x")
+    assert e.value.status == rp.RP_ERR_UNSUPPORTED

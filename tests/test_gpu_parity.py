@@ -1,0 +1,264 @@
+"""GPU parity: the HIP path through the C ABI against the fp64 oracle.
+
+Inputs are seeded and synthetic; every case prints its name before running.
+"""
+import sys
+import zlib
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from tests.gpu_util import compare, run_hip, run_oracle, to_host_out
+from tests.paged import bf16_bits, paged_from_dense, random_dense
+from workloads import CONFIGS, make_config_workload, make_workload
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(msg):
+    print(f"[case] {msg}", flush=True)
+    sys.stdout.flush()
+
+
+def test_config1_full():
+    _say("config1 full")
+    wl = make_config_workload(CONFIGS[1])
+    _, out, lse = run_hip(wl)
+    ref_out, ref_lse, _ = run_oracle(wl)
+    compare(out, lse, ref_out, ref_lse, "bf16", "config1")
+
+
+RAGGED = [
+    # (name, Hq, Hkv, d, seq_to_group, prefix_lens, resp_lens, kv_dtype)
+    ("edges-d128", 16, 8, 128, [0, 0, 0, 1, 1, 2, 2, 2, 2], [17, 64, 130],
+     [0, 1, 15, 16, 17, 255, 256, 257, 600], "bf16"),
+    ("edges-d64", 4, 2, 64, [0, 1, 1, 0, 2], [1, 16, 33], [31, 0, 513, 16, 2], "bf16"),
+    ("mha", 4, 4, 64, [0, 0, 1], [40, 3], [5, 70, 0], "bf16"),
+    ("nrep4", 8, 2, 128, [0, 0, 0, 1], [48, 80], [10, 300, 0, 47], "bf16"),
+    ("nrep8", 8, 1, 128, [0, 1, 0], [20, 70], [9, 129, 1], "bf16"),
+    ("big-group-3-passes", 16, 8, 128, [0] * 20 + [1] * 3, [70, 18], list(range(0, 230, 10)), "bf16"),
+    ("empty-keys", 4, 2, 64, [0, 1, 1], [0, 5], [0, 0, 3], "bf16"),
+    ("no-prefix", 4, 2, 128, [0, 0], [0], [40, 1], "bf16"),
+    ("fp8-edges", 16, 8, 128, [0, 0, 1, 1, 1], [33, 200], [0, 16, 17, 300, 513], "fp8"),
+    ("fp8-d64-nrep4", 8, 2, 64, [0, 1, 0], [64, 9], [100, 31, 0], "fp8"),
+]
+
+
+@pytest.mark.parametrize("case", RAGGED, ids=[c[0] for c in RAGGED])
+def test_ragged_shapes(case):
+    name, Hq, Hkv, d, s2g, P, L, dt = case
+    _say(name)
+    wl = make_workload(num_q_heads=Hq, num_kv_heads=Hkv, head_dim=d, seq_to_group=s2g,
+                       prefix_lens=P, resp_lens=L, seed=zlib.crc32(name.encode()) % 1000, kv_dtype=dt)
+    _, out, lse = run_hip(wl)
+    ref_out, ref_lse, _ = run_oracle(wl)
+    compare(out, lse, ref_out, ref_lse, dt, name)
+
+
+@pytest.mark.parametrize("kv_dtype", ["bf16", "fp8"])
+def test_random_group_map_many_groups(kv_dtype):
+    _say(f"random map {kv_dtype}")
+    rng = np.random.default_rng(77)
+    G = 37
+    s2g = rng.integers(0, G, size=150)
+    wl = make_workload(num_q_heads=16, num_kv_heads=8, head_dim=128, seq_to_group=s2g,
+                       prefix_lens=rng.integers(0, 300, size=G), resp_lens=rng.integers(0, 700, size=150),
+                       seed=5, kv_dtype=kv_dtype)
+    _, out, lse = run_hip(wl)
+    ref_out, ref_lse, _ = run_oracle(wl)
+    compare(out, lse, ref_out, ref_lse, kv_dtype, "random-map")
+
+
+@pytest.mark.parametrize("kv_dtype", ["bf16", "fp8"])
+def test_append_bytes_match_oracle_then_attention(kv_dtype):
+    _say(f"append {kv_dtype}")
+    rng = np.random.default_rng(11)
+    S = 40
+    L = rng.integers(0, 200, size=S)
+    L[:6] = [0, 15, 16, 31, 32, 47]
+    wl = make_workload(num_q_heads=16, num_kv_heads=8, head_dim=128, seq_to_group=np.arange(S) // 8,
+                       prefix_lens=[64, 100, 7, 16, 33], resp_lens=L, seed=9, append=True,
+                       kv_dtype=kv_dtype)
+    if kv_dtype == "fp8":  # make some appends grow the page scale (requantise path)
+        wl.k_new[::3] = bf16_bits(oracle.bf16_to_f32(wl.k_new[::3]) * np.float32(40.0))
+    batch, out, lse = run_hip(wl)
+    ref_out, ref_lse, pool = run_oracle(wl)
+    kp, vp, ks, vs = pool
+    torch.cuda.synchronize()
+    if kv_dtype == "fp8":
+        assert np.array_equal(batch.k_pages.cpu().numpy(), kp)
+        assert np.array_equal(batch.v_pages.cpu().numpy(), vp)
+        assert np.array_equal(batch.k_scale.cpu().numpy(), ks)
+        assert np.array_equal(batch.v_scale.cpu().numpy(), vs)
+    else:
+        assert np.array_equal(batch.k_pages.view(torch.int16).cpu().numpy().view(np.uint16), kp)
+        assert np.array_equal(batch.v_pages.view(torch.int16).cpu().numpy().view(np.uint16), vp)
+    compare(out, lse, ref_out, ref_lse, kv_dtype, f"append-{kv_dtype}")
+    # The append is idempotent: a second step changes nothing.
+    batch.step()
+    out2, lse2 = to_host_out(batch)
+    assert np.array_equal(out, out2) and np.array_equal(lse, lse2)
+
+
+def test_zero_query_gives_log_key_count():
+    """q = 0: lse = ln N exactly up to fp32, which pins the number of keys read."""
+    _say("q=0 key count")
+    rng = np.random.default_rng(3)
+    S = 24
+    wl = make_workload(num_q_heads=16, num_kv_heads=8, head_dim=128, seq_to_group=np.arange(S) // 8,
+                       prefix_lens=[100, 255, 17], resp_lens=rng.integers(0, 3000, size=S), seed=1)
+    wl.q[:] = 0
+    _, out, lse = run_hip(wl)
+    N = np.array([wl.prefix_lens[wl.seq_to_group[s]] + wl.resp_lens[s] for s in range(S)])
+    np.testing.assert_allclose(lse, np.log(N)[:, None].repeat(16, 1), rtol=0, atol=2e-5)
+    ref_out, ref_lse, _ = run_oracle(wl)
+    compare(out, lse, ref_out, ref_lse, "bf16", "q=0")
+
+
+def test_dominant_key_sweep_every_slot():
+    """One key per sequence dominates; sweeping it over every prefix and response slot
+    checks that each slot is read, with its own value row."""
+    _say("dominant key sweep")
+    d, P, L = 128, 40, 37
+    rng = np.random.default_rng(4)
+    pk, pv, rk, rv, s2g, _ = random_dense(rng, S=1, G=1, Hq=2, Hkv=1, d=d, prefix_lens=[P], resp_lens=[L])
+    # One sequence per slot: all share the prefix, each has its own response copy.
+    N = P + L
+    S = N
+    zero = bf16_bits(np.zeros((1, 1, d)))
+    one = bf16_bits(np.full((1, d), 1.0))
+    rks = []
+    seq_group = []
+    groups_pk, groups_pv = [], []
+    for t in range(N):
+        kp_ = np.repeat(zero, P, 0).copy()
+        kr_ = np.repeat(zero, L, 0).copy()
+        if t < P:
+            kp_[t, 0] = one
+        else:
+            kr_[t - P, 0] = one
+        groups_pk.append(kp_)
+        groups_pv.append(pv[0])
+        rks.append(kr_)
+        seq_group.append(t)
+    q = bf16_bits(np.full((S, 2, d), 1.0))      # score of the hot key: 128 / sqrt(128) = 11.3
+    wl = paged_from_dense(groups_pk, groups_pv, rks, [rv[0]] * S, np.array(seq_group), q,
+                          num_kv_heads=1, seed=2)
+    _, out, lse = run_hip(wl)
+    ref_out, ref_lse = oracle.attention_for_workload(wl)
+    compare(out, lse, ref_out, ref_lse, "bf16", "dominant-key")
+
+
+def test_physical_page_permutation_bitwise_and_determinism():
+    _say("page permutation")
+    rng = np.random.default_rng(8)
+    pk, pv, rk, rv, s2g, q = random_dense(rng, S=12, G=3, Hq=16, Hkv=8, d=128,
+                                          prefix_lens=[70, 33, 160],
+                                          resp_lens=list(rng.integers(0, 400, size=12)))
+    wl1 = paged_from_dense(pk, pv, rk, rv, s2g, q, num_kv_heads=8, seed=1)
+    wl2 = paged_from_dense(pk, pv, rk, rv, s2g, q, num_kv_heads=8, seed=2, pad_pages=7)
+    b1, o1, l1 = run_hip(wl1)
+    _, o2, l2 = run_hip(wl2)
+    assert np.array_equal(o1, o2) and np.array_equal(l1, l2)
+    b1.step()
+    o3, l3 = to_host_out(b1)
+    assert np.array_equal(o1, o3) and np.array_equal(l1, l3)
+
+
+def test_shared_prefix_equals_duplicated_prefix_on_gpu():
+    _say("shared vs duplicated prefix")
+    rng = np.random.default_rng(12)
+    S, G = 16, 2
+    P, L = [100, 45], list(rng.integers(0, 300, size=S))
+    pk, pv, rk, rv, s2g, q = random_dense(rng, S=S, G=G, Hq=16, Hkv=8, d=128, prefix_lens=P,
+                                          resp_lens=L, seq_to_group=np.arange(S) % G)
+    shared = paged_from_dense(pk, pv, rk, rv, s2g, q, num_kv_heads=8, seed=3)
+    empty = [pk[0][:0]] * S
+    dup = paged_from_dense(empty, empty, [np.concatenate([pk[s2g[s]], rk[s]]) for s in range(S)],
+                           [np.concatenate([pv[s2g[s]], rv[s]]) for s in range(S)], np.arange(S), q,
+                           num_kv_heads=8, seed=4)
+    _, o1, l1 = run_hip(shared)
+    _, o2, l2 = run_hip(dup)
+    # Different split points and MFMA vs VALU arithmetic: equal within rounding.
+    assert np.abs(o1 - o2).max() <= 1e-2
+    assert np.abs(l1 - l2).max() <= 1e-4
+
+
+def test_fp8_all_codes_decode_like_the_oracle():
+    """A single key: out = decoded V codes * v_scale exactly (bf16 holds every e4m3 value)."""
+    _say("fp8 256 codes")
+    codes = np.arange(256, dtype=np.uint8)
+    codes[codes == 0x7F] = 0x7E      # NaN codes are not attention inputs
+    codes[codes == 0xFF] = 0xFE
+    wl = make_workload(num_q_heads=2, num_kv_heads=1, head_dim=128, seq_to_group=[0, 0],
+                       prefix_lens=[0], resp_lens=[1, 1], seed=0, kv_dtype="fp8")
+    for s in range(2):
+        page = wl.resp_block_table[s, 0]
+        wl.v_pages[page, 0, 0, :] = codes[s * 128:(s + 1) * 128]
+        wl.v_scale[page, 0] = np.float32(1.0)
+        wl.k_scale[page, 0] = np.float32(0.5)
+    _, out, lse = run_hip(wl)
+    ref_out, ref_lse, _ = run_oracle(wl)
+    want = oracle.e4m3_to_f64(codes).reshape(2, 1, 128)
+    assert np.array_equal(out[:, 0:1, :], want) and np.array_equal(out[:, 1:2, :], want)
+    assert np.array_equal(ref_out, np.repeat(want, 2, axis=1))
+    np.testing.assert_allclose(lse, ref_lse, rtol=0, atol=1e-5)
+
+
+def test_lse_combine_abi_against_oracle():
+    _say("lse_combine")
+    import paper_2606_26997_amd as rp
+    rng = np.random.default_rng(5)
+    rows, d = 300, 128
+    counts = rng.integers(0, 9, size=rows)
+    offs = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    n = int(offs[-1])
+    o = rng.standard_normal((n, d)).astype(np.float32)
+    l = (rng.standard_normal(n) * 3).astype(np.float32)
+    l[rng.random(n) < 0.1] = -np.inf
+    o[l == -np.inf] = np.nan           # an empty part's o must not be read into the sum
+    ref_out, ref_lse = oracle.lse_combine(o.astype(np.float64), l.astype(np.float64), offs)
+    dev = lambda x: torch.from_numpy(x).cuda()
+    out = torch.zeros((rows, d), dtype=torch.bfloat16, device="cuda")
+    lse = torch.zeros(rows, dtype=torch.float32, device="cuda")
+    rp.lse_combine(dev(o), dev(l), dev(offs), rows, d, out, lse)
+    torch.cuda.synchronize()
+    got = out.float().cpu().numpy().astype(np.float64)
+    gl = lse.cpu().numpy().astype(np.float64)
+    fin = np.isfinite(ref_lse)
+    assert np.all(gl[~fin] == -np.inf) and np.all(got[~fin] == 0)
+    assert np.abs(got - ref_out).max() <= 1e-2
+    assert np.abs(gl[fin] - ref_lse[fin]).max() <= 1e-5
+
+
+def test_validate_layout_reports_bad_page():
+    _say("validate_layout")
+    import paper_2606_26997_amd as rp
+    wl = make_workload(num_q_heads=4, num_kv_heads=2, head_dim=64, seq_to_group=[0, 0],
+                       prefix_lens=[20], resp_lens=[5, 40], seed=1)
+    batch = rp.DeviceBatch.from_workload(wl)
+    batch.validate()
+    batch.resp_block_table[1, 2] = wl.num_pages + 5
+    with pytest.raises(rp.RpError) as e:
+        batch.validate()
+    assert e.value.status == rp.RP_ERR_LAYOUT and "resp_block_table" in str(e.value)
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("cid", [2, 3, 4, 5])
+def test_full_config_sampled_rows(cid):
+    """Full-size configs in the bench launch configuration; oracle on sampled sequences."""
+    _say(f"config{cid} full size, sampled rows")
+    wl = make_config_workload(CONFIGS[cid])
+    _say(f"config{cid} generated: {wl.num_seqs} seqs, {wl.num_pages} pages")
+    _, out, lse = run_hip(wl)
+    rng = np.random.default_rng(cid)
+    S = wl.num_seqs
+    L = wl.attn_resp_lens
+    picks = {int(np.argmax(L)), int(np.argmin(L))} | set(rng.choice(S, size=min(12, S), replace=False).tolist())
+    seqs = sorted(picks)
+    ref_out, ref_lse, _ = run_oracle(wl, seqs=seqs)
+    compare(out[seqs], lse[seqs], ref_out, ref_lse, wl.kv_dtype, f"config{cid}")
+    assert np.isfinite(out).all() and np.isfinite(lse).all()
