@@ -1,0 +1,283 @@
+#!/usr/bin/env python3
+"""Benchmark: group decode attention over a paged, group-shared KV cache on one MI355X.
+
+One step = one decode-attention pass of one layer over the whole batch: the KV
+append (for workloads that carry new tokens), the work plan, the group-prefix
+parts, the response parts and the LSE combine, each one kernel launched through
+the C ABI on torch's current stream. HIP events between the launches give
+per-kernel times; the wall clock over K steps (synchronised on both sides)
+gives ms_per_step. Inputs are seeded synthetic data resident in HBM before the
+timed region starts.
+
+value = algorithmic bytes per step / step time (GB/s). Algorithmic bytes: each
+group's prompt-prefix K/V once (for groups with live members), every
+sequence's response K/V (including an appended token), q, out and lse, plus for
+an append the new k/v read and written, plus 8 bytes of fp8 scales per
+(page, kv-head) read. Plan, partial results and block tables are overhead.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "decode-attn achieved HBM GB/s (% of MI355X peak) + seq-steps/s per layer"
+HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E, vendor figure
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_attn_parts_config2.json")
+KERNEL_SOURCES = ["paper_2606_26997_amd/csrc/rp_attn.hip", "paper_2606_26997_amd/csrc/rp_device.h",
+                  "paper_2606_26997_amd/csrc/rp_internal.h"]
+
+
+def parse_args():
+    p = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=100)
+    p.add_argument("--warmup", type=int, default=10)
+    p.add_argument("--config", type=int, default=2, help="workload number 1-5 (default 2)")
+    p.add_argument("--seed", type=int, default=None)
+    p.add_argument("--cpu-seconds", type=float, default=15.0,
+                   help="wall-clock budget of the oracle CPU baseline sample (0 disables it)")
+    p.add_argument("--copy-calibration", action="store_true",
+                   help="run only a plain device copy of known size (for HBM counter scaling)")
+    p.add_argument("--traffic-from", metavar="DIR", default=None,
+                   help="summarise rocprofv3 --pmc runs under DIR (pmc_fetch, pmc_write, pmc_copy_fetch, "
+                        "pmc_copy_write) into the stored HBM traffic of the partial-attention kernel")
+    return p.parse_args()
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def byte_model(wl):
+    """Algorithmic bytes per step, split by the kernel that moves them."""
+    import numpy as np
+    S, Hq, Hkv, d = wl.num_seqs, wl.num_q_heads, wl.num_kv_heads, wl.head_dim
+    eb = wl.kv_elem_bytes
+    tok = Hkv * d * 2 * eb                       # K + V bytes of one token, all kv-heads
+    live = np.bincount(wl.seq_to_group, minlength=wl.num_groups) > 0
+    P = wl.prefix_lens.astype(np.int64)
+    L = wl.attn_resp_lens.astype(np.int64)
+    prefix_tokens = int(P[live].sum())
+    resp_tokens = int(L.sum())
+    q_bytes = S * Hq * d * 2
+    scale_bytes = 0
+    prefix_scale = resp_scale = 0
+    if wl.kv_dtype == "fp8":
+        prefix_scale = int(((P[live] + 15) // 16).sum()) * Hkv * 8
+        resp_scale = int(((L + 15) // 16).sum()) * Hkv * 8
+        scale_bytes = prefix_scale + resp_scale
+    append = 0
+    if wl.append:
+        append = S * Hkv * d * 2 * 2 + S * Hkv * d * 2 * eb
+    out = dict(prefix_kv=prefix_tokens * tok, resp_kv=resp_tokens * tok, q=q_bytes, out=S * Hq * d * 2,
+               lse=S * Hq * 4, scales=scale_bytes, append=append)
+    out["total"] = sum(out.values())
+    # The partial-attention kernel reads every K/V page once, their scales and q.
+    out["parts_kernel"] = out["prefix_kv"] + out["resp_kv"] + scale_bytes + q_bytes
+    out["prefix_tokens"], out["resp_tokens"] = prefix_tokens, resp_tokens
+    return out
+
+
+def load_traffic():
+    """HBM traffic of the partial-attention kernel from stored rocprofv3 counter runs, if current."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    with open(TRAFFIC_FILE) as f:
+        t = json.load(f)
+    if t.get("source_hash") != kernel_source_hash():
+        return None
+    return t.get("traffic_bytes_per_launch")
+
+
+def cpu_baseline(wl, budget_s, bytes_per_step):
+    """The oracle as it stands, single-threaded, on a bounded sample of sequences."""
+    if budget_s <= 0:
+        return None
+    import numpy as np
+    from threadpoolctl import threadpool_limits
+    import oracle
+    from oracle.append import append_for_workload
+
+    pool = None
+    t_app = 0.0
+    if wl.append:
+        t0 = time.perf_counter()
+        pool = append_for_workload(wl)
+        t_app = time.perf_counter() - t0
+    order = np.random.default_rng(0).permutation(wl.num_seqs)
+    done = 0
+    with threadpool_limits(limits=1):
+        t0 = time.perf_counter()
+        for s in order:
+            oracle.attention_for_workload(wl, seqs=[int(s)], pool=pool)
+            done += 1
+            if time.perf_counter() - t0 >= budget_s:
+                break
+        el = time.perf_counter() - t0
+    seq_steps_per_s = done / (el + t_app * done / wl.num_seqs)
+    return {"value": round(bytes_per_step / wl.num_seqs * seq_steps_per_s / 1e9, 4), "unit": "GB/s",
+            "cores": 1, "kind": "oracle",
+            "sample": f"fp64 numpy oracle on {done} of {wl.num_seqs} sequences (random order, "
+                      f"{el:.1f} s, 1 thread{', append on the whole pool' if wl.append else ''}); "
+                      f"scaled by the step's algorithmic bytes per sequence",
+            "seq_steps_per_s": round(seq_steps_per_s, 3)}
+
+
+def _pmc_kib_per_dispatch(csv_path, kernel_substr, counter):
+    import csv
+    vals = [float(r["Counter_Value"]) for r in csv.DictReader(open(csv_path))
+            if kernel_substr in r["Kernel_Name"] and r["Counter_Name"] == counter]
+    if not vals:
+        raise SystemExit(f"no {counter} rows for {kernel_substr} in {csv_path}")
+    return sum(vals) / len(vals), len(vals)
+
+
+def summarise_traffic(root):
+    """FETCH_SIZE / WRITE_SIZE (KiB per dispatch) of the partial-attention kernel, scaled by the
+    same counters' reading for a plain 1 GiB device copy (1 GiB read + 1 GiB written)."""
+    f = lambda sub: os.path.join(root, sub, "pmc_counter_collection.csv")
+    fetch, n1 = _pmc_kib_per_dispatch(f("pmc_fetch"), "attn_parts_kernel", "FETCH_SIZE")
+    write, n2 = _pmc_kib_per_dispatch(f("pmc_write"), "attn_parts_kernel", "WRITE_SIZE")
+    cfetch, _ = _pmc_kib_per_dispatch(f("pmc_copy_fetch"), "copyBuffer", "FETCH_SIZE")
+    cwrite, _ = _pmc_kib_per_dispatch(f("pmc_copy_write"), "copyBuffer", "WRITE_SIZE")
+    gib_kib = float(1 << 20)
+    kf, kw = gib_kib / cfetch, gib_kib / cwrite       # true bytes per counted byte
+    fetch_b, write_b = fetch * 1024 * kf, write * 1024 * kw
+    out = {"kernel": "attn_parts_kernel", "workload": "config2", "source_hash": kernel_source_hash(),
+           "fetch_kib_per_dispatch": round(fetch, 1), "write_kib_per_dispatch": round(write, 1),
+           "dispatches": [n1, n2], "copy_fetch_kib_per_GiB": round(cfetch, 1),
+           "copy_write_kib_per_GiB": round(cwrite, 1), "fetch_scale": round(kf, 4), "write_scale": round(kw, 4),
+           "read_bytes_per_launch": int(fetch_b), "write_bytes_per_launch": int(write_b),
+           "traffic_bytes_per_launch": int(fetch_b + write_b)}
+    print(json.dumps(out, indent=1))
+    return out
+
+
+def copy_calibration(steps):
+    import torch
+    n = 1 << 30
+    a = torch.empty(n, dtype=torch.uint8, device="cuda")
+    b = torch.empty_like(a)
+    a.fill_(1)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    el = (time.perf_counter() - t0) / steps
+    print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "ms": el * 1e3,
+                      "GBps_read_plus_write": 2 * n / el / 1e9}), flush=True)
+
+
+def main():
+    args = parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
+              f"(the attention shards exchange-free by whole groups, see the design notes).",
+              file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    if args.copy_calibration:
+        copy_calibration(args.steps)
+        return
+    if args.traffic_from:
+        summarise_traffic(args.traffic_from)
+        return
+
+    import paper_2606_26997_amd as rp
+    from workloads import CONFIGS, make_config_workload
+
+    cfg = CONFIGS[args.config]
+    t0 = time.perf_counter()
+    wl = make_config_workload(cfg, seed=args.seed)
+    gen_s = time.perf_counter() - t0
+    print(f"[bench] config{cfg.cid} generated in {gen_s:.1f}s: {wl.num_seqs} seqs, "
+          f"{wl.num_pages} pages", file=sys.stderr, flush=True)
+    torch.cuda.set_device(0)
+    batch = rp.DeviceBatch.from_workload(wl, device="cuda:0")
+    bm = byte_model(wl)
+
+    stages = (["append"] if wl.append else []) + ["plan", "parts", "combine"]
+    calls = {"append": batch.kv_append, "plan": batch.plan, "parts": batch.attn_parts,
+             "combine": batch.combine_parts}
+
+    def step(evs=None):
+        for i, name in enumerate(stages):
+            if evs is not None:
+                evs[i].record()
+            calls[name]()
+        if evs is not None:
+            evs[len(stages)].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(len(stages) + 1)]
+              for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        step(events[k])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_per_step = wall / args.steps * 1e3
+    per_kernel = {name: float(np.mean([events[k][i].elapsed_time(events[k][i + 1])
+                                       for k in range(args.steps)])) * 1e3
+                  for i, name in enumerate(stages)}      # microseconds
+    event_step_us = float(np.mean([events[k][0].elapsed_time(events[k][-1])
+                                   for k in range(args.steps)])) * 1e3
+
+    gbps = bm["total"] / (ms_per_step * 1e-3) / 1e9
+    parts_us = per_kernel["parts"]
+    achieved = bm["parts_kernel"] / (parts_us * 1e-6) / 1e9
+    traffic = load_traffic()
+    cpu = None
+    if args.cpu_seconds > 0:
+        print("[bench] timing the oracle CPU baseline", file=sys.stderr, flush=True)
+        cpu = cpu_baseline(wl, args.cpu_seconds, bm["total"])
+
+    line = {
+        "metric": METRIC,
+        "value": round(gbps, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.kv_dtype,
+        "data": "synthetic",
+        "config": {"workload": f"config{cfg.cid}: {cfg.name}", "seqs": wl.num_seqs,
+                   "groups": wl.num_groups, "q_heads": wl.num_q_heads, "kv_heads": wl.num_kv_heads,
+                   "head_dim": wl.head_dim, "page_size": wl.page_size, "kv_dtype": wl.kv_dtype,
+                   "append": wl.append, "prefix_tokens": bm["prefix_tokens"],
+                   "resp_tokens": bm["resp_tokens"], "seed": cfg.seed if args.seed is None else args.seed},
+        "pct_of_hbm_peak": round(100.0 * gbps / HBM_PEAK_GBPS, 2),
+        "seq_steps_per_s": round(wl.num_seqs / (ms_per_step * 1e-3), 1),
+        "algorithmic_bytes_per_step": int(bm["total"]),
+        "kernel_us": {k: round(v, 2) for k, v in per_kernel.items()},
+        "event_step_us": round(event_step_us, 2),
+        "roofline": {"kernel": "attn_parts_kernel", "bound": "hbm", "achieved": round(achieved, 2),
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                     "traffic": traffic, "algorithmic_bytes_per_launch": int(bm["parts_kernel"])},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

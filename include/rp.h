@@ -135,17 +135,17 @@ rp_status rp_group_decode_attn_workspace_size(const rp_paged_kv* kv,
  * workspace: device buffer of at least rp_group_decode_attn_workspace_size
  *   bytes, 256-byte aligned, used for the work plan and partial results;
  *   concurrent calls need distinct workspaces.
- * Equivalent to rp_plan + rp_attn_parts + rp_combine_parts. */
+ * Equivalent to rp_plan, rp_attn_parts, rp_combine_parts. */
 rp_status rp_group_decode_attn(const rp_paged_kv* kv, const rp_group_layout* layout,
                                const void* q, float softmax_scale, void* out, float* lse,
                                void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* Log-sum-exp merge of partial attention results over disjoint key subsets.
- * o_parts: fp32 [total_parts][head_dim], lse_parts: fp32 [total_parts] (natural
+ * o_parts: fp32 [total_parts][head_dim] (16-byte aligned), lse_parts: fp32 [total_parts] (natural
  * log, -inf marks an empty part whose o is ignored); row r owns parts
  * row_part_offsets[r] .. row_part_offsets[r+1]-1 (int32 CSR, [num_rows + 1]).
  *   lse_out[r] = ln sum_i exp(lse_i),  out[r] = sum_i exp(lse_i - lse_out[r]) o_i
- * out: bf16 [num_rows][head_dim]; lse_out: fp32 [num_rows] or NULL. A row with
+ * out: bf16 [num_rows][head_dim] (8-byte aligned); lse_out: fp32 [num_rows] or NULL. A row with
  * no non-empty part gets out = 0, lse = -inf. head_dim in {64, 128}. */
 rp_status rp_lse_combine(const float* o_parts, const float* lse_parts,
                          const int32_t* row_part_offsets, int32_t num_rows, int32_t head_dim,
@@ -155,15 +155,18 @@ rp_status rp_lse_combine(const float* o_parts, const float* lse_parts,
  * A decode step's layout is shared by every layer, so a caller can plan once
  * and run the attention of all layers against the same plan. */
 
-/* Build the work plan (group member lists, work items, CSR of partial results
- * per (sequence, query head)) in `workspace` from the layout's device arrays.
- * Must be re-run whenever seq_to_group, prefix_lens or resp_lens change. */
+/* Build the work plan (group member lists, prefix work items, response work
+ * items ordered longest first) in `workspace` from the layout's device arrays.
+ * Must be re-run whenever seq_to_group, prefix_lens or resp_lens change.
+ * Supports num_groups <= 4096. */
 rp_status rp_plan(const rp_paged_kv* kv, const rp_group_layout* layout,
                   void* workspace, size_t workspace_bytes, hipStream_t stream);
 
-/* Compute all partial results for a planned workspace: the group-prefix parts
- * (each group's prefix read once for all its members' query rows) and the
- * response parts (split along each sequence's response pages). */
+/* All partial results for a planned workspace, in one kernel launch:
+ * group-prefix parts (each group's prompt prefix read once per kv-head and
+ * applied to all query rows of its live members on the matrix cores) and
+ * response parts (each sequence's own response pages in fixed page chunks).
+ * q and softmax_scale as in rp_group_decode_attn. */
 rp_status rp_attn_parts(const rp_paged_kv* kv, const rp_group_layout* layout,
                         const void* q, float softmax_scale,
                         void* workspace, size_t workspace_bytes, hipStream_t stream);

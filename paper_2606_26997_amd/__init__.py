@@ -6,9 +6,10 @@ library has not been built.
 """
 from ._binding import (EXPORTED, LIB_PATH, RP_ERR_HIP, RP_ERR_INVALID_ARG, RP_ERR_LAYOUT,
                        RP_ERR_UNSUPPORTED, RP_ERR_WORKSPACE, RP_KV_BF16, RP_KV_FP8_E4M3, RP_OK,
-                       RpError, RpGroupLayout, RpPagedKV, attn_parts, combine_parts,
+                       RpError, RpGroupLayout, RpPagedKV, combine_parts,
                        group_decode_attn, group_decode_attn_workspace_size, group_layout,
-                       kv_append, last_error, load, lse_combine, paged_kv, plan, status_string,
+                       kv_append, last_error, load, lse_combine, paged_kv, plan, attn_parts,
+                       status_string,
                        validate_layout)
 from .batch import DeviceBatch
 

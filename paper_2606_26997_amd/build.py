@@ -14,9 +14,13 @@ LIB = os.path.join(PKG, "librp.so")
 SOURCES = ["rp_api.hip", "rp_plan.hip", "rp_attn.hip", "rp_combine.hip", "rp_append.hip"]
 ARCH = "gfx950"
 
-# Packed-fp32 VALU instructions are disabled for all device code.
+# Packed-fp32 VALU instructions are disabled for all device code. MFMA
+# accumulators are kept in ordinary VGPRs so that the prefix path of the
+# partial-attention kernel does not add accumulation registers on top of the
+# response path's budget.
 HIPCC_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Wall",
                "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+               "-mllvm", "-amdgpu-mfma-vgpr-form",
                "-I", INCLUDE, "-I", CSRC]
 
 

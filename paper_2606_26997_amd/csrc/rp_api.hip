@@ -80,6 +80,8 @@ rp_status check_shape(const rp_paged_kv* kv, const rp_group_layout* l, Shape* sh
   }
   // Every index the kernels form stays below 2^31 elements per int32 table.
   const long long rows = (long long)l->num_seqs * l->num_q_heads;
+  if (l->num_seqs > 0 && l->num_groups > rp::kPlanMaxGroups)
+    return fail(RP_ERR_UNSUPPORTED, "num_groups %d above the planner's limit %d", l->num_groups, rp::kPlanMaxGroups);
   if ((long long)l->num_seqs * l->max_resp_pages >= (1ll << 31) ||
       (long long)l->num_groups * l->max_prefix_pages >= (1ll << 31) || rows >= (1ll << 31))
     return fail(RP_ERR_UNSUPPORTED, "layout too large for int32 indexing");
@@ -98,7 +100,7 @@ rp_status check_shape(const rp_paged_kv* kv, const rp_group_layout* l, Shape* sh
 
 // Workspace layout, 256-byte aligned sections.
 struct WsLayout {
-  size_t hdr, grp_count, grp_fill, grp_off, members, pitems, ritems, row_offs, part_o, part_lse, total;
+  size_t hdr, grp_off, members, pitems, ritems, rpage0, part_o, part_lse, total;
   long long max_pitems, max_ritems, max_parts;
   int max_pc, max_rc;
 };
@@ -107,7 +109,7 @@ size_t align_up(size_t x) { return (x + 255) & ~size_t(255); }
 
 bool ws_layout(const Shape& sh, WsLayout* w) {
   w->max_pc = rp::cdiv(sh.max_pp, rp::kPrefixChunkPages);
-  w->max_rc = rp::cdiv(sh.max_rp, rp::kRespChunkPages);
+  w->max_rc = rp::cdiv(sh.max_rp, rp::kRespChunkPagesMin);
   const long long groups_used = sh.G < sh.S ? sh.G : sh.S;
   w->max_pitems = groups_used * w->max_pc;
   w->max_ritems = (long long)sh.S * w->max_rc;
@@ -117,13 +119,11 @@ bool ws_layout(const Shape& sh, WsLayout* w) {
     return false;
   size_t o = 0;
   w->hdr = o;       o = align_up(o + sizeof(int) * rp::kHdrSlots);
-  w->grp_count = o; o = align_up(o + sizeof(int) * (size_t)sh.G);
-  w->grp_fill = o;  o = align_up(o + sizeof(int) * (size_t)sh.G);
   w->grp_off = o;   o = align_up(o + sizeof(int) * ((size_t)sh.G + 1));
   w->members = o;   o = align_up(o + sizeof(int) * (size_t)sh.S);
   w->pitems = o;    o = align_up(o + sizeof(int2) * (size_t)w->max_pitems);
-  w->ritems = o;    o = align_up(o + sizeof(int2) * (size_t)w->max_ritems);
-  w->row_offs = o;  o = align_up(o + sizeof(int) * ((size_t)sh.S * sh.Hq + 1));
+  w->ritems = o;    o = align_up(o + sizeof(int4) * (size_t)w->max_ritems);
+  w->rpage0 = o;    o = align_up(o + sizeof(int) * (size_t)w->max_ritems);
   w->part_o = o;    o = align_up(o + sizeof(float) * (size_t)w->max_parts * sh.D);
   w->part_lse = o;  o = align_up(o + sizeof(float) * (size_t)w->max_parts);
   w->total = o;
@@ -134,18 +134,19 @@ rp::PlanView plan_view(void* ws, const WsLayout& w) {
   char* b = static_cast<char*>(ws);
   rp::PlanView v;
   v.hdr = reinterpret_cast<int*>(b + w.hdr);
-  v.grp_count = reinterpret_cast<int*>(b + w.grp_count);
-  v.grp_fill = reinterpret_cast<int*>(b + w.grp_fill);
   v.grp_off = reinterpret_cast<int*>(b + w.grp_off);
   v.grp_members = reinterpret_cast<int*>(b + w.members);
   v.prefix_items = reinterpret_cast<int2*>(b + w.pitems);
-  v.resp_items = reinterpret_cast<int2*>(b + w.ritems);
-  v.row_offs = reinterpret_cast<int*>(b + w.row_offs);
+  v.resp_items = reinterpret_cast<int4*>(b + w.ritems);
+  v.resp_first_page = reinterpret_cast<int*>(b + w.rpage0);
   v.part_o = reinterpret_cast<float*>(b + w.part_o);
   v.part_lse = reinterpret_cast<float*>(b + w.part_lse);
   v.max_prefix_chunks = w.max_pc;
   v.max_resp_chunks = w.max_rc;
+  v.parts_per_row = w.max_pc + w.max_rc;
   v.max_parts = (int)w.max_parts;
+  v.max_prefix_items = (int)w.max_pitems;
+  v.max_resp_items = (int)w.max_ritems;
   return v;
 }
 
@@ -232,6 +233,8 @@ rp_status rp_plan(const rp_paged_kv* kv, const rp_group_layout* l, void* ws, siz
   a.seq_to_group = l->seq_to_group;
   a.prefix_lens = l->prefix_lens;
   a.resp_lens = l->resp_lens;
+  a.resp_block_table = l->resp_block_table;
+  a.num_pages = sh.num_pages;
   a.max_prefix_pages = sh.max_pp;
   a.max_resp_pages = sh.max_rp;
   a.view = plan_view(ws, w);
@@ -248,11 +251,8 @@ rp_status rp_attn_parts(const rp_paged_kv* kv, const rp_group_layout* l, const v
   if (st != RP_OK || sh.S == 0) return st;
   if (q == nullptr || !aligned(q, 16)) return fail(RP_ERR_INVALID_ARG, "q must be non-NULL and 16-byte aligned");
   const rp::AttnArgs a = attn_args(kv, l, q, softmax_scale, plan_view(ws, w));
-  hipError_t e = rp::launch_prefix_parts(a, sh.D, sh.nrep, sh.fp8, w.max_pitems, stream);
-  if (e != hipSuccess) return hip_fail(e, "prefix kernel launch");
-  e = rp::launch_resp_parts(a, sh.D, sh.nrep, sh.fp8, w.max_ritems, stream);
-  if (e != hipSuccess) return hip_fail(e, "response kernel launch");
-  return RP_OK;
+  hipError_t e = rp::launch_attn_parts(a, sh.D, sh.nrep, sh.fp8, w.max_pitems, w.max_ritems, stream);
+  return e == hipSuccess ? RP_OK : hip_fail(e, "attention parts kernel launch");
 }
 
 rp_status rp_combine_parts(const rp_paged_kv* kv, const rp_group_layout* l, void* out, float* lse, void* ws,
@@ -265,13 +265,24 @@ rp_status rp_combine_parts(const rp_paged_kv* kv, const rp_group_layout* l, void
   if (out == nullptr || !aligned(out, 16)) return fail(RP_ERR_INVALID_ARG, "out must be non-NULL and 16-byte aligned");
   if (lse != nullptr && !aligned(lse, 4)) return fail(RP_ERR_INVALID_ARG, "lse must be 4-byte aligned");
   const rp::PlanView v = plan_view(ws, w);
-  rp::CombineArgs c;
+  rp::CombineArgs c{};
   c.o_parts = v.part_o;
   c.lse_parts = v.part_lse;
-  c.row_offs = v.row_offs;
+  c.row_offs = nullptr;
   c.num_rows = sh.S * sh.Hq;
   c.out = out;
   c.lse = lse;
+  c.plan_hdr = v.hdr;
+  c.num_q_heads = sh.Hq;
+  c.num_groups = sh.G;
+  c.parts_per_row = v.parts_per_row;
+  c.max_prefix_pages = sh.max_pp;
+  c.max_resp_pages = sh.max_rp;
+  c.max_prefix_chunks = v.max_prefix_chunks;
+  c.max_resp_chunks = v.max_resp_chunks;
+  c.seq_to_group = l->seq_to_group;
+  c.prefix_lens = l->prefix_lens;
+  c.resp_lens = l->resp_lens;
   hipError_t e = rp::launch_combine(c, sh.D, stream);
   return e == hipSuccess ? RP_OK : hip_fail(e, "combine kernel launch");
 }
@@ -302,11 +313,11 @@ rp_status rp_lse_combine(const float* o_parts, const float* lse_parts, const int
   if (num_rows == 0) return RP_OK;
   if (row_part_offsets == nullptr || out == nullptr)
     return fail(RP_ERR_INVALID_ARG, "row_part_offsets/out is NULL");
-  if (!aligned(out, 4)) return fail(RP_ERR_INVALID_ARG, "out must be 4-byte aligned");
+  if (!aligned(out, 8)) return fail(RP_ERR_INVALID_ARG, "out must be 8-byte aligned");
   if (lse_out != nullptr && !aligned(lse_out, 4)) return fail(RP_ERR_INVALID_ARG, "lse_out must be 4-byte aligned");
-  if ((o_parts != nullptr && !aligned(o_parts, 8)) || (lse_parts != nullptr && !aligned(lse_parts, 4)))
-    return fail(RP_ERR_INVALID_ARG, "o_parts must be 8-byte and lse_parts 4-byte aligned");
-  rp::CombineArgs c;
+  if ((o_parts != nullptr && !aligned(o_parts, 16)) || (lse_parts != nullptr && !aligned(lse_parts, 4)))
+    return fail(RP_ERR_INVALID_ARG, "o_parts must be 16-byte and lse_parts 4-byte aligned");
+  rp::CombineArgs c{};
   c.o_parts = o_parts;
   c.lse_parts = lse_parts;
   c.row_offs = row_part_offsets;

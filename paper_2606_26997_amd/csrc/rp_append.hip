@@ -37,9 +37,7 @@ __device__ void append_fp8_head(uint8_t* blk, float* scale_slot, int r, const ui
       uint8_t* row = blk + (size_t)rr * D + lane * EPL;
 #pragma unroll
       for (int e = 0; e < EPL; ++e) {
-        float v, unused;
-        e4m3x2_to_f32_scaled((uint32_t)row[e], false, v, unused);
-        const float val = (v * kE4m3DecodeScale) * old;  // the first product is exact
+        const float val = e4m3_to_f32(row[e]) * old;
         row[e] = (uint8_t)f32_to_e4m3(val / scale);
       }
     }

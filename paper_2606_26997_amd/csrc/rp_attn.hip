@@ -1,22 +1,29 @@
-// Partial attention over planned work items.
+// Partial attention over planned work items, in one launch. Work units are
+// (item, kv-head) pairs, one per one-wave block: all group-prefix units first,
+// then the response units longest first, so the hardware dispatcher hands the
+// last free slots the smallest units.
 //
-// Group-prefix items (MFMA): every response of a GRPO group is sampled from the
-// same prompt, so the group's prompt-prefix KV is read once per (group, kv-head,
-// chunk) and applied to all of the group's query rows at once: live members x
-// (Hq / Hkv) query heads, as 16-row tiles on the bf16 MFMA
-//   S^T = K Q^T   (M = 16 tokens, N = 16 query rows, K = head_dim)
-//   O^T = V^T P^T (M = 16 head_dim columns, N = 16 query rows, K = 32 tokens)
-// with fp32 accumulation and an online softmax over the chunk.
+// Group-prefix units (MFMA): every response of a GRPO group is sampled from
+// the same prompt, so the group's prompt-prefix KV is read once per (group,
+// kv-head, chunk) and applied to all of the group's query rows at once: live
+// members x (Hq / Hkv) query heads as 16-row tiles, one page per step:
+//   S^T  = K Q^T   on mfma 16x16x32 bf16 (M = 16 tokens, N = 16 rows, K = 32 of head_dim)
+//   O^T += V^T P^T on mfma 16x16x16 bf16 (M = 16 head_dim columns, N = 16 rows, K = 16 tokens)
+// with fp32 accumulation and an online softmax; the page's V goes through LDS
+// to feed the transposed operand.
 //
-// Response items (VALU): each (sequence, kv-head, chunk of response pages) is
-// one wave. A (page, kv-head) block is contiguous in the pool and is read with
-// fully coalesced 16-byte loads: lane l holds EPL head_dim elements of token
+// Response units (VALU): one (sequence, chunk of response pages, kv-head). A
+// (page, kv-head) block is contiguous in the pool and is read with fully
+// coalesced 16-byte loads: lane l holds EPL head_dim elements of token
 // (load * TPL + l / LPT). Scores are reduced over the LPT lanes of a token with
-// DPP, and every group of LPT lanes keeps its own online-softmax state over its
-// tokens; the states are merged once at the end of the item.
+// DPP, every group of LPT lanes keeps its own online-softmax state, and the
+// states are merged once per unit. Page loads are software-pipelined: the next
+// page's K is requested as soon as this page's scores exist and its V as soon as
+// this page's V is unpacked. The response chunk length (pages per unit) is
+// chosen by the planner for the batch.
 //
-// Each item writes one partial (o normalised, lse natural-log) per query row
-// into the plan's CSR slot; the combine kernel merges the parts of a row.
+// Each unit writes one partial (o normalised, lse natural-log) per query row
+// into its fixed slot (row, chunk); the combine kernel merges a row's parts.
 #include "rp_device.h"
 #include "rp_internal.h"
 
@@ -34,14 +41,18 @@ struct RespGeom {
   static constexpr int TPL = 64 / LPT;            // tokens per load instruction
   static constexpr int LOADS = kPage / TPL;       // loads per (page, kv-head) block
   static constexpr int BLOCK_BYTES = kPage * D * EB;
+  static constexpr int QW = EPL / 8;              // uint4 words of bf16 q per lane per row
 };
 
+__device__ inline float dot2_bf16(uint32_t a, uint32_t b, float acc) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a), __builtin_bit_cast(bf16x2_t, b), acc,
+                                         false);
+}
 __device__ inline float dot8_bf16(const uint4& a, const uint4& b, float acc) {
-  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a.x), __builtin_bit_cast(bf16x2_t, b.x), acc, false);
-  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a.y), __builtin_bit_cast(bf16x2_t, b.y), acc, false);
-  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a.z), __builtin_bit_cast(bf16x2_t, b.z), acc, false);
-  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a.w), __builtin_bit_cast(bf16x2_t, b.w), acc, false);
-  return acc;
+  acc = dot2_bf16(a.x, b.x, acc);
+  acc = dot2_bf16(a.y, b.y, acc);
+  acc = dot2_bf16(a.z, b.z, acc);
+  return dot2_bf16(a.w, b.w, acc);
 }
 
 __device__ inline void unpack_bf16x8(const uint4& w, float* f) {
@@ -51,192 +62,50 @@ __device__ inline void unpack_bf16x8(const uint4& w, float* f) {
   f[6] = bf16_lo(w.w); f[7] = bf16_hi(w.w);
 }
 
-// 16 e4m3 codes -> 16 floats scaled by 2^-8 (exact).
-__device__ inline void unpack_e4m3x16(const uint4& w, float* f) {
-  e4m3x2_to_f32_scaled(w.x, false, f[0], f[1]);
-  e4m3x2_to_f32_scaled(w.x, true, f[2], f[3]);
-  e4m3x2_to_f32_scaled(w.y, false, f[4], f[5]);
-  e4m3x2_to_f32_scaled(w.y, true, f[6], f[7]);
-  e4m3x2_to_f32_scaled(w.z, false, f[8], f[9]);
-  e4m3x2_to_f32_scaled(w.z, true, f[10], f[11]);
-  e4m3x2_to_f32_scaled(w.w, false, f[12], f[13]);
-  e4m3x2_to_f32_scaled(w.w, true, f[14], f[15]);
-}
-
-template <int D, int NREP, bool FP8>
-__global__ __launch_bounds__(64) void resp_parts_kernel(const AttnArgs a) {
-  using G = RespGeom<D, FP8>;
-  constexpr int EPL = G::EPL, LPT = G::LPT, TPL = G::TPL, LOADS = G::LOADS;
-  const int Hkv = a.num_kv_heads;
-  const int item = blockIdx.x / Hkv;
-  const int h = blockIdx.x - item * Hkv;
-  if (item >= a.view.hdr[kHdrRespItems]) return;
-
-  const int2 it = a.view.resp_items[item];
-  const int s = min(max(it.x, 0), a.num_seqs - 1);
-  const int c = min(max(it.y, 0), a.view.max_resp_chunks - 1);
-  const int L = clamp_len(a.resp_lens[s], a.max_resp_pages);
-  const int g = clamp_group(a.seq_to_group[s], a.num_groups);
-  const int npc = prefix_chunks(a.prefix_lens[g], a.max_prefix_pages, a.view.max_prefix_chunks);
-  const int tok0 = c * (kRespChunkPages * kPage);
-  const int ntok = min(kRespChunkPages * kPage, L - tok0);
-  const int npages = cdiv(ntok, kPage);
-  const int lane = threadIdx.x;
-  const int tg = lane / LPT;
-  const int sub = lane - tg * LPT;
-
-  // This lane's EPL head_dim elements of the NREP query rows of kv-head h.
-  const uint16_t* qrow = reinterpret_cast<const uint16_t*>(a.q) +
-                         ((size_t)s * a.num_q_heads + (size_t)h * NREP) * D + sub * EPL;
-  uint4 qb[NREP];
-  float qf[FP8 ? NREP : 1][FP8 ? EPL : 1];
-#pragma unroll
-  for (int r = 0; r < NREP; ++r) {
-    if constexpr (!FP8) {
-      qb[r] = *reinterpret_cast<const uint4*>(qrow + (size_t)r * D);
-    } else {
-      const uint4 lo = *reinterpret_cast<const uint4*>(qrow + (size_t)r * D);
-      const uint4 hi = *reinterpret_cast<const uint4*>(qrow + (size_t)r * D + 8);
-      unpack_bf16x8(lo, &qf[r][0]);
-      unpack_bf16x8(hi, &qf[r][8]);
-    }
-  }
-
-  float m[NREP], l[NREP], o[NREP][EPL];
-#pragma unroll
-  for (int r = 0; r < NREP; ++r) {
-    m[r] = -INFINITY;
-    l[r] = 0.f;
-#pragma unroll
-    for (int e = 0; e < EPL; ++e) o[r][e] = 0.f;
-  }
-
-  const int* bt = a.resp_block_table + (size_t)s * a.max_resp_pages + c * kRespChunkPages;
-  const char* kpool = static_cast<const char*>(a.k_pages);
-  const char* vpool = static_cast<const char*>(a.v_pages);
-
-  for (int p = 0; p < npages; ++p) {
-    const int page = clamp_page(bt[p], a.num_pages);
-    const size_t blk = ((size_t)page * Hkv + h) * G::BLOCK_BYTES + (size_t)lane * 16;
-    uint4 kr[LOADS], vr[LOADS];
-#pragma unroll
-    for (int i = 0; i < LOADS; ++i) kr[i] = *reinterpret_cast<const uint4*>(kpool + blk + i * 1024);
-#pragma unroll
-    for (int i = 0; i < LOADS; ++i) vr[i] = *reinterpret_cast<const uint4*>(vpool + blk + i * 1024);
-
-    const int nvalid = min(kPage, ntok - p * kPage);
-    float smul = a.qk_scale, vmul = 1.f;
-    if constexpr (FP8) {
-      smul *= a.k_scale[(size_t)page * Hkv + h] * kE4m3DecodeScale;
-      vmul = a.v_scale[(size_t)page * Hkv + h] * kE4m3DecodeScale;
-    }
-
-    float sc[LOADS][NREP];
-#pragma unroll
-    for (int i = 0; i < LOADS; ++i) {
-      if constexpr (!FP8) {
-#pragma unroll
-        for (int r = 0; r < NREP; ++r) sc[i][r] = group_sum<LPT>(dot8_bf16(qb[r], kr[i], 0.f)) * smul;
-      } else {
-        float kf[EPL];
-        unpack_e4m3x16(kr[i], kf);
-#pragma unroll
-        for (int r = 0; r < NREP; ++r) {
-          float acc = 0.f;
-#pragma unroll
-          for (int e = 0; e < EPL; ++e) acc = fmaf(qf[r][e], kf[e], acc);
-          sc[i][r] = group_sum<LPT>(acc) * smul;
-        }
-      }
-    }
-
-    float vf[LOADS][EPL];
-#pragma unroll
-    for (int i = 0; i < LOADS; ++i) {
-      if constexpr (!FP8) unpack_bf16x8(vr[i], vf[i]);
-      else unpack_e4m3x16(vr[i], vf[i]);
-    }
-
-    if (nvalid < kPage) {  // ragged last page: padding rows may hold anything
-#pragma unroll
-      for (int i = 0; i < LOADS; ++i) {
-        const bool ok = i * TPL + tg < nvalid;
-#pragma unroll
-        for (int r = 0; r < NREP; ++r) sc[i][r] = ok ? sc[i][r] : -INFINITY;
-#pragma unroll
-        for (int e = 0; e < EPL; ++e) vf[i][e] = ok ? vf[i][e] : 0.f;
-      }
-    }
-
-#pragma unroll
-    for (int r = 0; r < NREP; ++r) {
-      float mx = m[r];
-#pragma unroll
-      for (int i = 0; i < LOADS; ++i) mx = fmaxf(mx, sc[i][r]);
-      const float mu = mx == -INFINITY ? 0.f : mx;
-      const float alpha = fast_exp2(m[r] - mu);
-      float pw[LOADS], ps = 0.f;
-#pragma unroll
-      for (int i = 0; i < LOADS; ++i) {
-        pw[i] = fast_exp2(sc[i][r] - mu);
-        ps += pw[i];
-      }
-      l[r] = l[r] * alpha + ps;
-      m[r] = mx;
-#pragma unroll
-      for (int e = 0; e < EPL; ++e) o[r][e] *= alpha;
-#pragma unroll
-      for (int i = 0; i < LOADS; ++i) {
-        const float pv = pw[i] * vmul;
-#pragma unroll
-        for (int e = 0; e < EPL; ++e) o[r][e] = fmaf(pv, vf[i][e], o[r][e]);
-      }
-    }
-  }
-
-  // Merge the TPL lane groups' states and write one partial per query row.
-  const int row0 = s * a.num_q_heads + h * NREP;
-#pragma unroll
-  for (int r = 0; r < NREP; ++r) {
-    const float M = xor_max_from<LPT>(m[r]);
-    const float Mu = M == -INFINITY ? 0.f : M;
-    const float w = fast_exp2(m[r] - Mu);
-    const float lt = xor_sum_from<LPT>(l[r] * w);
-    const float inv = 1.f / lt;
-    float oo[EPL];
-#pragma unroll
-    for (int e = 0; e < EPL; ++e) oo[e] = xor_sum_from<LPT>(o[r][e] * w) * inv;
-    const int part = clamp_part(a.view.row_offs[row0 + r] + npc + c, a.view.max_parts);
-    if (tg == 0) {
-      float4* dst = reinterpret_cast<float4*>(a.view.part_o + (size_t)part * D + sub * EPL);
-#pragma unroll
-      for (int e = 0; e < EPL; e += 4) dst[e / 4] = make_float4(oo[e], oo[e + 1], oo[e + 2], oo[e + 3]);
-    }
-    if (lane == 0) a.view.part_lse[part] = (M + fast_log2(lt)) * kLn2;
-  }
-}
-
-// ---------------------------------------------------------------------------
-// Group-prefix path (MFMA 16x16x32 bf16)
-// ---------------------------------------------------------------------------
-__device__ inline f32x4_t mfma16x16x32(const bf16x8_t& a, const bf16x8_t& b, const f32x4_t& c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
-}
-
 // Two floats known to be exact in bf16 -> packed bf16 pair (truncation is exact).
 __device__ inline uint32_t pack_exact_bf16x2(float lo, float hi) {
   return (__float_as_uint(lo) >> 16) | (__float_as_uint(hi) & 0xFFFF0000u);
 }
 
-// 8 e4m3 codes -> 8 bf16 values scaled by 2^-8 (exact).
+// 4 e4m3 codes -> 4 exact floats (gfx950 converts OCP e4m3fn in hardware).
+__device__ inline void e4m3x4_to_f32(uint32_t w, float* f) {
+  const auto lo = __builtin_amdgcn_cvt_pk_f32_fp8((int)w, false);
+  const auto hi = __builtin_amdgcn_cvt_pk_f32_fp8((int)w, true);
+  f[0] = lo[0];
+  f[1] = lo[1];
+  f[2] = hi[0];
+  f[3] = hi[1];
+}
+__device__ inline void unpack_e4m3x16(const uint4& w, float* f) {
+  e4m3x4_to_f32(w.x, f);
+  e4m3x4_to_f32(w.y, f + 4);
+  e4m3x4_to_f32(w.z, f + 8);
+  e4m3x4_to_f32(w.w, f + 12);
+}
+// 8 e4m3 codes -> 8 bf16 values (exact: every e4m3 value is a bf16 value).
 __device__ inline uint4 e4m3x8_to_bf16x8(uint32_t w0, uint32_t w1) {
   float f[8];
-  e4m3x2_to_f32_scaled(w0, false, f[0], f[1]);
-  e4m3x2_to_f32_scaled(w0, true, f[2], f[3]);
-  e4m3x2_to_f32_scaled(w1, false, f[4], f[5]);
-  e4m3x2_to_f32_scaled(w1, true, f[6], f[7]);
+  e4m3x4_to_f32(w0, f);
+  e4m3x4_to_f32(w1, f + 4);
   return make_uint4(pack_exact_bf16x2(f[0], f[1]), pack_exact_bf16x2(f[2], f[3]),
                     pack_exact_bf16x2(f[4], f[5]), pack_exact_bf16x2(f[6], f[7]));
+}
+
+template <int D, bool FP8>
+__device__ inline size_t resp_block(const AttnArgs& a, int page, int h, int lane) {
+  return ((size_t)page * a.num_kv_heads + h) * RespGeom<D, FP8>::BLOCK_BYTES + (size_t)lane * 16;
+}
+
+// ---------------------------------------------------------------------------
+// Group-prefix path
+// ---------------------------------------------------------------------------
+__device__ inline f32x4_t mfma16x16x32(const bf16x8_t& a, const bf16x8_t& b, const f32x4_t& c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+__device__ inline f32x4_t mfma16x16x16(const bf16x4_t& a, const bf16x4_t& b, const f32x4_t& c) {
+  typedef short s16x4_t __attribute__((ext_vector_type(4)));
+  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4_t, a), __builtin_bit_cast(s16x4_t, b),
+                                                   c, 0, 0, 0);
 }
 
 // A operand of S^T = K Q^T for one page: lane (r16, quad) holds K[token r16][kb*32 + quad*8 + 0..7].
@@ -255,11 +124,10 @@ __device__ inline void load_k_operand(const char* pool, size_t blk_bytes, int r1
   }
 }
 
-// Copy one page's V block (bf16, or fp8 decoded to bf16 * 2^-8) into LDS rows
-// [row0, row0 + 16); rows at or beyond `nvalid` are written as zeros.
+// Copy one page's V block (bf16, or fp8 decoded to bf16) into LDS rows
+// 0..15; rows at or beyond `nvalid` are written as zeros.
 template <int D, bool FP8, int STRIDE>
-__device__ inline void stage_v(const char* pool, size_t blk_bytes, int nvalid, uint16_t* vt, int row0,
-                               int lane) {
+__device__ inline void stage_v(const char* pool, size_t blk_bytes, int nvalid, uint16_t* vt, int lane) {
   if constexpr (!FP8) {
 #pragma unroll
     for (int i = 0; i < kPage * D * 2 / 1024; ++i) {
@@ -267,7 +135,7 @@ __device__ inline void stage_v(const char* pool, size_t blk_bytes, int nvalid, u
       const int tok = e0 / D, col = e0 % D;
       uint4 w = make_uint4(0, 0, 0, 0);
       if (tok < nvalid) w = *reinterpret_cast<const uint4*>(pool + blk_bytes + (size_t)e0 * 2);
-      uint2* dst = reinterpret_cast<uint2*>(vt + (row0 + tok) * STRIDE + col);
+      uint2* dst = reinterpret_cast<uint2*>(vt + tok * STRIDE + col);
       dst[0] = make_uint2(w.x, w.y);
       dst[1] = make_uint2(w.z, w.w);
     }
@@ -282,7 +150,7 @@ __device__ inline void stage_v(const char* pool, size_t blk_bytes, int nvalid, u
         lo = e4m3x8_to_bf16x8(w.x, w.y);
         hi = e4m3x8_to_bf16x8(w.z, w.w);
       }
-      uint2* dst = reinterpret_cast<uint2*>(vt + (row0 + tok) * STRIDE + col);
+      uint2* dst = reinterpret_cast<uint2*>(vt + tok * STRIDE + col);
       dst[0] = make_uint2(lo.x, lo.y);
       dst[1] = make_uint2(lo.z, lo.w);
       dst[2] = make_uint2(hi.x, hi.y);
@@ -291,21 +159,19 @@ __device__ inline void stage_v(const char* pool, size_t blk_bytes, int nvalid, u
   }
 }
 
+// One group-prefix unit: kv-head h of (group, chunk of prefix pages), for all
+// query rows of the group's live members, 16 rows per pass and one page per
+// step. A group with more than 16 query rows reads the chunk again for each
+// further pass; the chunk (a few tens of KiB) is then still in this XCD's L2.
 template <int D, int NREP, bool FP8>
-__global__ __launch_bounds__(64) void prefix_parts_kernel(const AttnArgs a) {
+__device__ void prefix_unit(const AttnArgs& a, int item, int h, uint16_t* vt) {
   constexpr int KB = D / 32;       // MFMA k-blocks over head_dim
   constexpr int DT = D / 16;       // 16-column output tiles over head_dim
-  constexpr int T = kPrefixTiles;  // 16-row query tiles per pass
   constexpr int STRIDE = D + 4;    // staged V row pitch (bf16 elements)
   constexpr int EB = FP8 ? 1 : 2;
   constexpr size_t BLOCK_BYTES = (size_t)kPage * D * EB;
-  __shared__ __attribute__((aligned(16))) uint16_t vt[2 * kPage * STRIDE];
 
   const int Hkv = a.num_kv_heads;
-  const int item = blockIdx.x / Hkv;
-  const int h = blockIdx.x - item * Hkv;
-  if (item >= a.view.hdr[kHdrPrefixItems]) return;
-
   const int2 it = a.view.prefix_items[item];
   const int g = clamp_group(it.x, a.num_groups);
   const int c = min(max(it.y, 0), a.view.max_prefix_chunks - 1);
@@ -322,180 +188,294 @@ __global__ __launch_bounds__(64) void prefix_parts_kernel(const AttnArgs a) {
   const char* vpool = static_cast<const char*>(a.v_pages);
   const uint16_t* qall = static_cast<const uint16_t*>(a.q);
 
-  for (int r0 = 0; r0 < R; r0 += 16 * T) {
-    const int ntiles = min(T, cdiv(R - r0, 16));
-    bf16x8_t qop[T][KB];
-    int rowid[T];
+  for (int r0 = 0; r0 < R; r0 += 16) {
+    const int rr = r0 + r16;
+    int rowid = -1;
+    if (rr < R) {
+      const int mem = rr / NREP, rep = rr - mem * NREP;
+      const int sq = min(max(a.view.grp_members[moff + mem], 0), a.num_seqs - 1);
+      rowid = sq * a.num_q_heads + h * NREP + rep;
+    }
+    bf16x8_t qop[KB];
 #pragma unroll
-    for (int t = 0; t < T; ++t) {
-      const int rr = r0 + t * 16 + r16;
-      rowid[t] = -1;
-      if (t < ntiles && rr < R) {
-        const int mem = rr / NREP, rep = rr - mem * NREP;
-        const int sq = min(max(a.view.grp_members[moff + mem], 0), a.num_seqs - 1);
-        rowid[t] = sq * a.num_q_heads + h * NREP + rep;
-      }
-#pragma unroll
-      for (int kb = 0; kb < KB; ++kb) {
-        uint4 w = make_uint4(0, 0, 0, 0);
-        if (rowid[t] >= 0)
-          w = *reinterpret_cast<const uint4*>(qall + (size_t)rowid[t] * D + kb * 32 + quad * 8);
-        qop[t][kb] = __builtin_bit_cast(bf16x8_t, w);
-      }
+    for (int kb = 0; kb < KB; ++kb) {
+      uint4 w = make_uint4(0, 0, 0, 0);
+      if (rowid >= 0) w = *reinterpret_cast<const uint4*>(qall + (size_t)rowid * D + kb * 32 + quad * 8);
+      qop[kb] = __builtin_bit_cast(bf16x8_t, w);
     }
 
-    float mrow[T], lrow[T];
-    f32x4_t oacc[T][DT];
+    float mrow = -INFINITY, lrow = 0.f;
+    f32x4_t oacc[DT];
 #pragma unroll
-    for (int t = 0; t < T; ++t) {
-      mrow[t] = -INFINITY;
-      lrow[t] = 0.f;
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) oacc[t][dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    }
+    for (int dt = 0; dt < DT; ++dt) oacc[dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-    for (int pb = 0; pb < npages; pb += 2) {
-      const bool has_b = pb + 1 < npages;
-      const int nva = min(kPage, ntok - pb * kPage);
-      const int nvb = has_b ? min(kPage, ntok - (pb + 1) * kPage) : 0;
-      const int pa = clamp_page(bt[pb], a.num_pages);
-      const int pbp = has_b ? clamp_page(bt[pb + 1], a.num_pages) : pa;
-      const size_t blk_a = ((size_t)pa * Hkv + h) * BLOCK_BYTES;
-      const size_t blk_b = ((size_t)pbp * Hkv + h) * BLOCK_BYTES;
+    for (int p = 0; p < npages; ++p) {
+      const int nv = min(kPage, ntok - p * kPage);
+      const int pg = clamp_page(bt[p], a.num_pages);
+      const size_t blk = ((size_t)pg * Hkv + h) * BLOCK_BYTES;
 
-      bf16x8_t ka[KB], kbop[KB];
-      load_k_operand<D, FP8>(kpool, blk_a, r16, quad, ka);
-      load_k_operand<D, FP8>(kpool, blk_b, r16, quad, kbop);
+      __syncthreads();  // the previous page's LDS reads are complete
+      stage_v<D, FP8, STRIDE>(vpool, blk, nv, vt, lane);
 
-      __syncthreads();  // the previous block's LDS reads are complete
-      stage_v<D, FP8, STRIDE>(vpool, blk_a, nva, vt, 0, lane);
-      stage_v<D, FP8, STRIDE>(vpool, blk_b, nvb, vt, kPage, lane);
-      __syncthreads();
-
-      float sa = a.qk_scale, sb = a.qk_scale, va = 1.f, vb = 1.f;
+      float sm = a.qk_scale, vm = 1.f;
       if constexpr (FP8) {
-        sa *= a.k_scale[(size_t)pa * Hkv + h] * kE4m3DecodeScale;
-        sb *= a.k_scale[(size_t)pbp * Hkv + h] * kE4m3DecodeScale;
-        va = a.v_scale[(size_t)pa * Hkv + h] * kE4m3DecodeScale;
-        vb = a.v_scale[(size_t)pbp * Hkv + h] * kE4m3DecodeScale;
+        sm *= a.k_scale[(size_t)pg * Hkv + h];
+        vm = a.v_scale[(size_t)pg * Hkv + h];
       }
-
-      bf16x8_t pop[T];
+      // Entry i of this lane is token quad*4+i of the page and query row r16 of the tile.
+      f32x4_t sacc = {0.f, 0.f, 0.f, 0.f};
+      {
+        bf16x8_t kop[KB];
+        load_k_operand<D, FP8>(kpool, blk, r16, quad, kop);
 #pragma unroll
-      for (int t = 0; t < T; ++t) {
-        if (t >= ntiles) continue;
-        f32x4_t s_a = {0.f, 0.f, 0.f, 0.f}, s_b = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int kb = 0; kb < KB; ++kb) {
-          s_a = mfma16x16x32(ka[kb], qop[t][kb], s_a);
-          s_b = mfma16x16x32(kbop[kb], qop[t][kb], s_b);
-        }
-        // Entry i of this lane is token quad*4+i of the page, query row r16 of the tile.
-        float x[8];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          x[i] = quad * 4 + i < nva ? s_a[i] * sa : -INFINITY;
-          x[4 + i] = quad * 4 + i < nvb ? s_b[i] * sb : -INFINITY;
-        }
-        float mloc = x[0];
-#pragma unroll
-        for (int k = 1; k < 8; ++k) mloc = fmaxf(mloc, x[k]);
-        mloc = xor_max_from<16>(mloc);
-        const float mx = fmaxf(mrow[t], mloc);
-        const float mu = mx == -INFINITY ? 0.f : mx;
-        const float alpha = fast_exp2(mrow[t] - mu);
-        float pw[8], ps = 0.f;
-#pragma unroll
-        for (int k = 0; k < 8; ++k) {
-          pw[k] = fast_exp2(x[k] - mu);
-          ps += pw[k];
-        }
-        lrow[t] = lrow[t] * alpha + ps;
-        mrow[t] = mx;
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt) oacc[t][dt] *= alpha;
-        // B operand of O^T = V^T P^T: k-slot quad*8+j is token quad*4+j of page a
-        // (j < 4) or of page b (j >= 4): exactly this lane's eight probabilities.
-        const uint4 pk = make_uint4(pack_bf16x2(pw[0] * va, pw[1] * va), pack_bf16x2(pw[2] * va, pw[3] * va),
-                                    pack_bf16x2(pw[4] * vb, pw[5] * vb), pack_bf16x2(pw[6] * vb, pw[7] * vb));
-        pop[t] = __builtin_bit_cast(bf16x8_t, pk);
+        for (int kb = 0; kb < KB; ++kb) sacc = mfma16x16x32(kop[kb], qop[kb], sacc);
       }
+      float x[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) x[i] = quad * 4 + i < nv ? sacc[i] * sm : -INFINITY;
+      float mloc = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
+      mloc = xor_max_from<16>(mloc);
+      const float mx = fmaxf(mrow, mloc);
+      const float mu = mx == -INFINITY ? 0.f : mx;
+      const float alpha = fast_exp2(mrow - mu);
+      float pw[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) pw[i] = fast_exp2(x[i] - mu);
+      lrow = lrow * alpha + ((pw[0] + pw[1]) + (pw[2] + pw[3]));
+      mrow = mx;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) oacc[dt] *= alpha;
+      // B operand of O^T = V^T P^T: k-slot quad*4+j is token quad*4+j of the
+      // page, i.e. exactly this lane's four probabilities.
+      const bf16x4_t pop = __builtin_bit_cast(
+          bf16x4_t, make_uint2(pack_bf16x2(pw[0] * vm, pw[1] * vm), pack_bf16x2(pw[2] * vm, pw[3] * vm)));
 
+      __syncthreads();  // the staged V is visible to the whole wave
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) {
-        // A operand: V^T[column dt*16 + r16][k-slot quad*8 + j], same token order as the B operand.
-        const uint16_t* col = vt + dt * 16 + r16;
-        const int ta = quad * 4, tb = kPage + quad * 4;
-        uint32_t w[4];
-        w[0] = (uint32_t)col[(ta + 0) * STRIDE] | ((uint32_t)col[(ta + 1) * STRIDE] << 16);
-        w[1] = (uint32_t)col[(ta + 2) * STRIDE] | ((uint32_t)col[(ta + 3) * STRIDE] << 16);
-        w[2] = (uint32_t)col[(tb + 0) * STRIDE] | ((uint32_t)col[(tb + 1) * STRIDE] << 16);
-        w[3] = (uint32_t)col[(tb + 2) * STRIDE] | ((uint32_t)col[(tb + 3) * STRIDE] << 16);
-        const bf16x8_t vop = __builtin_bit_cast(bf16x8_t, make_uint4(w[0], w[1], w[2], w[3]));
-#pragma unroll
-        for (int t = 0; t < T; ++t)
-          if (t < ntiles) oacc[t][dt] = mfma16x16x32(vop, pop[t], oacc[t][dt]);
+        // A operand: V^T[column dt*16 + r16][k-slot quad*4 + j] = V[token quad*4 + j][column].
+        const uint16_t* col = vt + (quad * 4) * STRIDE + dt * 16 + r16;
+        const uint32_t w0 = (uint32_t)col[0] | ((uint32_t)col[STRIDE] << 16);
+        const uint32_t w1 = (uint32_t)col[2 * STRIDE] | ((uint32_t)col[3 * STRIDE] << 16);
+        oacc[dt] = mfma16x16x16(__builtin_bit_cast(bf16x4_t, make_uint2(w0, w1)), pop, oacc[dt]);
       }
     }
 
-#pragma unroll
-    for (int t = 0; t < T; ++t) {
-      if (t >= ntiles) continue;
-      const float lt = xor_sum_from<16>(lrow[t]);
-      if (rowid[t] < 0) continue;
-      const int part = clamp_part(a.view.row_offs[rowid[t]] + c, a.view.max_parts);
+    const float lt = xor_sum_from<16>(lrow);
+    if (rowid >= 0) {
+      const int part = clamp_part(rowid * a.view.parts_per_row + c, a.view.max_parts);
       const float inv = 1.f / lt;
       float* dst = a.view.part_o + (size_t)part * D + quad * 4;
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) {
-        const f32x4_t v = oacc[t][dt] * inv;
+        const f32x4_t v = oacc[dt] * inv;
         *reinterpret_cast<float4*>(dst + dt * 16) = make_float4(v[0], v[1], v[2], v[3]);
       }
-      if (quad == 0) a.view.part_lse[part] = (mrow[t] + fast_log2(lt)) * kLn2;
+      if (quad == 0) a.view.part_lse[part] = (mrow + fast_log2(lt)) * kLn2;
     }
   }
 }
 
+// ---------------------------------------------------------------------------
+// The kernel
+// ---------------------------------------------------------------------------
+// One response unit: kv-head h of response item `item`.
 template <int D, int NREP, bool FP8>
-hipError_t launch_one_resp(const AttnArgs& a, long long blocks, hipStream_t st) {
-  resp_parts_kernel<D, NREP, FP8><<<dim3((unsigned)blocks), dim3(64), 0, st>>>(a);
-  return hipGetLastError();
+__device__ void resp_unit(const AttnArgs& a, int item, int h) {
+  using G = RespGeom<D, FP8>;
+  constexpr int EPL = G::EPL, LPT = G::LPT, TPL = G::TPL, LOADS = G::LOADS, QW = G::QW;
+  const int Hkv = a.num_kv_heads;
+  const int lane = threadIdx.x;
+  const int tg = lane / LPT;
+  const int sub = lane - tg * LPT;
+  const char* kpool = static_cast<const char*>(a.k_pages);
+  const char* vpool = static_cast<const char*>(a.v_pages);
+
+  // The item record and its first page id come straight from the plan, so the
+  // first K/V loads depend on one load only.
+  const int4 m = a.view.resp_items[item];
+  const int s = min(max(m.x, 0), a.num_seqs - 1);
+  const int chunk = planned_chunk_pages(a.view.hdr);
+  const int c = min(max(m.y, 0), a.view.max_resp_chunks - 1);
+  const int npc = m.w;
+  const int ntok = min(chunk * kPage, min(m.z, a.max_resp_pages * kPage) - c * (chunk * kPage));
+  const int npages = cdiv(ntok, kPage);
+  int page = clamp_page(a.view.resp_first_page[item], a.num_pages);
+  uint4 kr[LOADS], vr[LOADS];
+  {
+    const size_t blk = resp_block<D, FP8>(a, page, h, lane);
+#pragma unroll
+    for (int i = 0; i < LOADS; ++i) kr[i] = *reinterpret_cast<const uint4*>(kpool + blk + i * 1024);
+#pragma unroll
+    for (int i = 0; i < LOADS; ++i) vr[i] = *reinterpret_cast<const uint4*>(vpool + blk + i * 1024);
+  }
+  const int* bt = a.resp_block_table + (size_t)s * a.max_resp_pages + c * chunk;
+
+  // This lane's EPL head_dim elements of the NREP query rows of kv-head h (bf16).
+  const uint16_t* qrow =
+      reinterpret_cast<const uint16_t*>(a.q) + ((size_t)s * a.num_q_heads + (size_t)h * NREP) * D + sub * EPL;
+  uint4 qb[NREP][QW];
+#pragma unroll
+  for (int r = 0; r < NREP; ++r)
+#pragma unroll
+    for (int w = 0; w < QW; ++w) qb[r][w] = *reinterpret_cast<const uint4*>(qrow + (size_t)r * D + w * 8);
+
+  float mrun[NREP], l[NREP], o[NREP][EPL];
+#pragma unroll
+  for (int r = 0; r < NREP; ++r) {
+    mrun[r] = -INFINITY;
+    l[r] = 0.f;
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) o[r][e] = 0.f;
+  }
+
+  for (int p = 0; p < npages; ++p) {
+    // The following page (this one again after the last: a cache hit).
+    const int next_page = p + 1 < npages ? clamp_page(bt[p + 1], a.num_pages) : page;
+    const size_t next_blk = resp_block<D, FP8>(a, next_page, h, lane);
+    const int nvalid = min(kPage, ntok - p * kPage);
+    float smul = a.qk_scale, vmul = 1.f;
+    if constexpr (FP8) {
+      smul *= a.k_scale[(size_t)page * Hkv + h];
+      vmul = a.v_scale[(size_t)page * Hkv + h];
+    }
+
+    float sc[LOADS][NREP];
+#pragma unroll
+    for (int i = 0; i < LOADS; ++i) {
+      if constexpr (!FP8) {
+#pragma unroll
+        for (int r = 0; r < NREP; ++r) sc[i][r] = group_sum<LPT>(dot8_bf16(qb[r][0], kr[i], 0.f)) * smul;
+      } else {
+        const uint4 k0 = e4m3x8_to_bf16x8(kr[i].x, kr[i].y);
+        const uint4 k1 = e4m3x8_to_bf16x8(kr[i].z, kr[i].w);
+#pragma unroll
+        for (int r = 0; r < NREP; ++r)
+          sc[i][r] = group_sum<LPT>(dot8_bf16(qb[r][1], k1, dot8_bf16(qb[r][0], k0, 0.f))) * smul;
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < LOADS; ++i) kr[i] = *reinterpret_cast<const uint4*>(kpool + next_blk + i * 1024);
+
+    float vf[LOADS][EPL];
+#pragma unroll
+    for (int i = 0; i < LOADS; ++i) {
+      if constexpr (!FP8) unpack_bf16x8(vr[i], vf[i]);
+      else unpack_e4m3x16(vr[i], vf[i]);
+    }
+#pragma unroll
+    for (int i = 0; i < LOADS; ++i) vr[i] = *reinterpret_cast<const uint4*>(vpool + next_blk + i * 1024);
+
+    if (nvalid < kPage) {  // ragged last page: padding rows may hold anything
+#pragma unroll
+      for (int i = 0; i < LOADS; ++i) {
+        const bool ok = i * TPL + tg < nvalid;
+#pragma unroll
+        for (int r = 0; r < NREP; ++r) sc[i][r] = ok ? sc[i][r] : -INFINITY;
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) vf[i][e] = ok ? vf[i][e] : 0.f;
+      }
+    }
+
+#pragma unroll
+    for (int r = 0; r < NREP; ++r) {
+      float mx = mrun[r];
+#pragma unroll
+      for (int i = 0; i < LOADS; ++i) mx = fmaxf(mx, sc[i][r]);
+      const float mu = mx == -INFINITY ? 0.f : mx;
+      const float alpha = fast_exp2(mrun[r] - mu);
+      float pw[LOADS], ps = 0.f;
+#pragma unroll
+      for (int i = 0; i < LOADS; ++i) {
+        pw[i] = fast_exp2(sc[i][r] - mu);
+        ps += pw[i];
+      }
+      l[r] = l[r] * alpha + ps;
+      mrun[r] = mx;
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) o[r][e] *= alpha;
+#pragma unroll
+      for (int i = 0; i < LOADS; ++i) {
+        const float pv = pw[i] * vmul;
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) o[r][e] = fmaf(pv, vf[i][e], o[r][e]);
+      }
+    }
+    page = next_page;
+  }
+
+  // Merge the TPL lane groups' states and write one partial per query row.
+  const int row0 = s * a.num_q_heads + h * NREP;
+#pragma unroll
+  for (int r = 0; r < NREP; ++r) {
+    const float M = xor_max_from<LPT>(mrun[r]);
+    const float Mu = M == -INFINITY ? 0.f : M;
+    const float w = fast_exp2(mrun[r] - Mu);
+    const float lt = xor_sum_from<LPT>(l[r] * w);
+    const float inv = 1.f / lt;
+    float oo[EPL];
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) oo[e] = xor_sum_from<LPT>(o[r][e] * w) * inv;
+    const int part = clamp_part((row0 + r) * a.view.parts_per_row + npc + c, a.view.max_parts);
+    if (tg == 0) {
+      float4* dst = reinterpret_cast<float4*>(a.view.part_o + (size_t)part * D + sub * EPL);
+#pragma unroll
+      for (int e = 0; e < EPL; e += 4) dst[e / 4] = make_float4(oo[e], oo[e + 1], oo[e + 2], oo[e + 3]);
+    }
+    if (lane == 0) a.view.part_lse[part] = (M + fast_log2(lt)) * kLn2;
+  }
 }
+
+// All partial results in one launch, one unit per one-wave block: the first
+// `prefix_blocks` blocks take group-prefix units (dispatched first, so their
+// short, latency-bound MFMA work overlaps the streaming response units), the
+// rest take response units in plan order (longest first). Blocks beyond the
+// planned counts exit at once. The item counts are clamped to the plan's
+// capacity, so even a workspace that was never planned cannot send a wave
+// outside the item lists.
 template <int D, int NREP, bool FP8>
-hipError_t launch_one_prefix(const AttnArgs& a, long long blocks, hipStream_t st) {
-  prefix_parts_kernel<D, NREP, FP8><<<dim3((unsigned)blocks), dim3(64), 0, st>>>(a);
+__global__ __launch_bounds__(64) void attn_parts_kernel(const AttnArgs a, int prefix_blocks) {
+  __shared__ __attribute__((aligned(16))) uint16_t vt[kPage * (D + 4)];
+  const int Hkv = a.num_kv_heads;
+  int b = blockIdx.x;
+  if (b < prefix_blocks) {
+    const int item = b / Hkv;
+    if (item < min(a.view.hdr[kHdrPrefixItems], a.view.max_prefix_items))
+      prefix_unit<D, NREP, FP8>(a, item, b - item * Hkv, vt);
+    return;
+  }
+  b -= prefix_blocks;
+  const int item = b / Hkv;
+  if (item < min(a.view.hdr[kHdrRespItems], a.view.max_resp_items)) resp_unit<D, NREP, FP8>(a, item, b - item * Hkv);
+}
+
+template <int D, int NREP, bool FP8>
+hipError_t launch_one(const AttnArgs& a, long long prefix_blocks, long long resp_blocks, hipStream_t st) {
+  attn_parts_kernel<D, NREP, FP8>
+      <<<dim3((unsigned)(prefix_blocks + resp_blocks)), dim3(64), 0, st>>>(a, (int)prefix_blocks);
   return hipGetLastError();
 }
 
-template <bool PREFIX, int D, bool FP8>
-hipError_t by_nrep(const AttnArgs& a, int n_rep, long long blocks, hipStream_t st) {
+template <int D, bool FP8>
+hipError_t by_nrep(const AttnArgs& a, int n_rep, long long pb, long long rb, hipStream_t st) {
   switch (n_rep) {
-    case 1: return PREFIX ? launch_one_prefix<D, 1, FP8>(a, blocks, st) : launch_one_resp<D, 1, FP8>(a, blocks, st);
-    case 2: return PREFIX ? launch_one_prefix<D, 2, FP8>(a, blocks, st) : launch_one_resp<D, 2, FP8>(a, blocks, st);
-    case 4: return PREFIX ? launch_one_prefix<D, 4, FP8>(a, blocks, st) : launch_one_resp<D, 4, FP8>(a, blocks, st);
-    case 8: return PREFIX ? launch_one_prefix<D, 8, FP8>(a, blocks, st) : launch_one_resp<D, 8, FP8>(a, blocks, st);
+    case 1: return launch_one<D, 1, FP8>(a, pb, rb, st);
+    case 2: return launch_one<D, 2, FP8>(a, pb, rb, st);
+    case 4: return launch_one<D, 4, FP8>(a, pb, rb, st);
+    case 8: return launch_one<D, 8, FP8>(a, pb, rb, st);
     default: return hipErrorInvalidValue;
   }
 }
 
-template <bool PREFIX>
-hipError_t dispatch(const AttnArgs& a, int head_dim, int n_rep, bool fp8, long long blocks, hipStream_t st) {
-  if (blocks <= 0) return hipSuccess;
-  if (head_dim == 128) return fp8 ? by_nrep<PREFIX, 128, true>(a, n_rep, blocks, st) : by_nrep<PREFIX, 128, false>(a, n_rep, blocks, st);
-  if (head_dim == 64) return fp8 ? by_nrep<PREFIX, 64, true>(a, n_rep, blocks, st) : by_nrep<PREFIX, 64, false>(a, n_rep, blocks, st);
-  return hipErrorInvalidValue;
-}
-
 }  // namespace
 
-hipError_t launch_prefix_parts(const AttnArgs& a, int head_dim, int n_rep, bool fp8, long long max_items,
-                               hipStream_t stream) {
-  return dispatch<true>(a, head_dim, n_rep, fp8, max_items * a.num_kv_heads, stream);
-}
-
-hipError_t launch_resp_parts(const AttnArgs& a, int head_dim, int n_rep, bool fp8, long long max_items,
-                             hipStream_t stream) {
-  return dispatch<false>(a, head_dim, n_rep, fp8, max_items * a.num_kv_heads, stream);
+hipError_t launch_attn_parts(const AttnArgs& a, int head_dim, int n_rep, bool fp8, long long max_prefix_items,
+                             long long max_resp_items, hipStream_t stream) {
+  const long long pb = max_prefix_items * a.num_kv_heads, rb = max_resp_items * a.num_kv_heads;
+  if (pb + rb <= 0) return hipSuccess;
+  if (head_dim == 128) return fp8 ? by_nrep<128, true>(a, n_rep, pb, rb, stream) : by_nrep<128, false>(a, n_rep, pb, rb, stream);
+  if (head_dim == 64) return fp8 ? by_nrep<64, true>(a, n_rep, pb, rb, stream) : by_nrep<64, false>(a, n_rep, pb, rb, stream);
+  return hipErrorInvalidValue;
 }
 
 }  // namespace rp

@@ -1,6 +1,9 @@
 // Log-sum-exp merge of partial results: one wave per output row.
 //   lse = ln sum_i exp(lse_i),  out = sum_i exp(lse_i - lse) o_i
-// Parts with lse_i = -inf are empty and their o_i is never read into the sum.
+// Parts with lse_i = -inf are empty and their o_i is never added. A row's
+// parts are read in batches: LPP lanes cover one part's head_dim with float4
+// loads, so one load instruction fetches 64 / LPP parts and a batch keeps
+// kBatch such loads in flight per wave.
 #include "rp_device.h"
 #include "rp_internal.h"
 
@@ -8,53 +11,75 @@ namespace rp {
 namespace {
 
 constexpr int kCombineWaves = 4;
+constexpr int kBatch = 8;
 
 template <int D>
 __global__ __launch_bounds__(64 * kCombineWaves) void combine_kernel(const CombineArgs a) {
-  constexpr int EPL = D / 64;  // output elements per lane
+  constexpr int LPP = D / 4;     // lanes per part
+  constexpr int PPI = 64 / LPP;  // parts per load instruction
   const int row = blockIdx.x * kCombineWaves + (threadIdx.x >> 6);
   if (row >= a.num_rows) return;
   const int lane = threadIdx.x & 63;
-  const int p0 = a.row_offs[row], p1 = a.row_offs[row + 1];
+  const int slot = lane / LPP, sub = lane - slot * LPP;
+
+  int p0, n;
+  if (a.row_offs != nullptr) {
+    p0 = a.row_offs[row];
+    n = a.row_offs[row + 1] - p0;
+  } else {
+    const int s = row / a.num_q_heads;
+    const int g = clamp_group(a.seq_to_group[s], a.num_groups);
+    n = prefix_chunks(a.prefix_lens[g], a.max_prefix_pages, a.max_prefix_chunks) +
+        resp_chunks(a.resp_lens[s], a.max_resp_pages, a.max_resp_chunks, planned_chunk_pages(a.plan_hdr));
+    p0 = row * a.parts_per_row;
+  }
 
   float mx = -INFINITY;
-  for (int p = p0 + lane; p < p1; p += 64) mx = fmaxf(mx, a.lse_parts[p]);
+  for (int i = lane; i < n; i += 64) mx = fmaxf(mx, a.lse_parts[p0 + i]);
   mx = xor_max_from<1>(mx);
 
-  float acc[EPL];
-#pragma unroll
-  for (int e = 0; e < EPL; ++e) acc[e] = 0.f;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
   float wsum = 0.f;
   if (mx != -INFINITY) {
-#pragma unroll 4
-    for (int p = p0; p < p1; ++p) {
-      const float lp = a.lse_parts[p];
-      const float w = fast_exp2((lp - mx) * kLog2e);  // 0 for an empty part
-      const float* src = a.o_parts + (size_t)p * D + lane * EPL;
-      float ov[EPL];
-      if constexpr (EPL == 2) {
-        const float2 t = *reinterpret_cast<const float2*>(src);
-        ov[0] = t.x;
-        ov[1] = t.y;
-      } else {
-        ov[0] = src[0];
-      }
-      const bool live = lp != -INFINITY;
-      wsum += w;
+    for (int base = 0; base < n; base += PPI * kBatch) {
+      float lp[kBatch];
+      float4 ov[kBatch];
 #pragma unroll
-      for (int e = 0; e < EPL; ++e) acc[e] = live ? fmaf(w, ov[e], acc[e]) : acc[e];
+      for (int b = 0; b < kBatch; ++b) {
+        const int k = base + b * PPI + slot;
+        lp[b] = -INFINITY;
+        ov[b] = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (k < n) {
+          lp[b] = a.lse_parts[p0 + k];
+          ov[b] = *reinterpret_cast<const float4*>(a.o_parts + (size_t)(p0 + k) * D + sub * 4);
+        }
+      }
+#pragma unroll
+      for (int b = 0; b < kBatch; ++b) {
+        const bool live = lp[b] != -INFINITY;
+        const float w = live ? fast_exp2((lp[b] - mx) * kLog2e) : 0.f;
+        wsum += w;
+        acc.x = live ? fmaf(w, ov[b].x, acc.x) : acc.x;
+        acc.y = live ? fmaf(w, ov[b].y, acc.y) : acc.y;
+        acc.z = live ? fmaf(w, ov[b].z, acc.z) : acc.z;
+        acc.w = live ? fmaf(w, ov[b].w, acc.w) : acc.w;
+      }
     }
   }
+  acc.x = xor_sum_from<LPP>(acc.x);
+  acc.y = xor_sum_from<LPP>(acc.y);
+  acc.z = xor_sum_from<LPP>(acc.z);
+  acc.w = xor_sum_from<LPP>(acc.w);
+  wsum = xor_sum_from<LPP>(wsum);
 
-  uint16_t* out = static_cast<uint16_t*>(a.out) + (size_t)row * D + lane * EPL;
-  const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
-  if constexpr (EPL == 2) {
-    *reinterpret_cast<uint32_t*>(out) = pack_bf16x2(acc[0] * inv, acc[1] * inv);
-  } else {
-    out[0] = (uint16_t)f32_to_bf16_bits(acc[0] * inv);
+  if (slot == 0) {
+    const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
+    uint2 packed;
+    packed.x = pack_bf16x2(acc.x * inv, acc.y * inv);
+    packed.y = pack_bf16x2(acc.z * inv, acc.w * inv);
+    *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.out) + (size_t)row * D + sub * 4) = packed;
   }
-  if (a.lse != nullptr && lane == 0)
-    a.lse[row] = wsum > 0.f ? mx + fast_log2(wsum) * kLn2 : -INFINITY;
+  if (a.lse != nullptr && lane == 0) a.lse[row] = wsum > 0.f ? mx + fast_log2(wsum) * kLn2 : -INFINITY;
 }
 
 }  // namespace

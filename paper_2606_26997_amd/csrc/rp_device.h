@@ -9,39 +9,57 @@ namespace rp {
 
 // Tokens per KV page (the only page size the kernels are built for).
 constexpr int kPage = 16;
-// Pages per response work item (split-KV chunk) and per prefix work item.
-constexpr int kRespChunkPages = 16;
+// Pages per prefix work item, and the range of pages per response work item
+// (split-KV chunk). The planner picks the response chunk for each batch: the
+// short one when the average response is below kLongResponsePages pages, the
+// long one otherwise (longer chunks amortise each unit's start-up latency;
+// shorter ones keep the end of the launch balanced). Workspace is sized for
+// the short chunk.
 constexpr int kPrefixChunkPages = 4;
-// Query-row tiles (16 rows each) one prefix wave keeps in registers per pass.
-constexpr int kPrefixTiles = 2;
+constexpr int kRespChunkPagesMin = 32;
+constexpr int kRespChunkPagesMax = 64;
+constexpr int kLongResponsePages = 256;
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
 // Plan header slots.
-enum : int { kHdrPrefixItems = 0, kHdrRespItems = 1, kHdrParts = 2, kHdrSlots = 16 };
+enum : int {
+  kHdrPrefixItems = 0,
+  kHdrRespItems = 1,
+  kHdrFullRespItems = 2,
+  kHdrRespChunkPages = 3,
+  kHdrSlots = 16
+};
+// Largest group count the planner keeps in LDS.
+constexpr int kPlanMaxGroups = 4096;
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 __host__ __device__ inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 
-// Pointers into a planned workspace (all device memory).
+// Pointers into a planned workspace (all device memory). Partial results of
+// query row r = s * Hq + j live in slots r * parts_per_row + k: first the
+// group's prefix chunks (k < prefix chunks of the group), then the sequence's
+// response chunks.
 struct PlanView {
   int* hdr;            // [kHdrSlots]
-  int* grp_count;      // [G]  live members per group
-  int* grp_fill;       // [G]  placement cursor
   int* grp_off;        // [G+1] CSR of members
-  int* grp_members;    // [S]
+  int* grp_members;    // [S]   members of each group in ascending order of arrival
   int2* prefix_items;  // [max_prefix_items]  (group, chunk)
-  int2* resp_items;    // [max_resp_items]    (sequence, chunk)
-  int* row_offs;       // [S*Hq + 1] CSR of partial results per (sequence, query head)
-  float* part_o;       // [max_parts][D]
-  float* part_lse;     // [max_parts]
+  int4* resp_items;    // [max_resp_items]    (sequence, chunk, clamped length, prefix chunks), longest first
+  int* resp_first_page;  // [max_resp_items]  physical page of each response item's first page
+  float* part_o;       // [S*Hq*parts_per_row][D]
+  float* part_lse;     // [S*Hq*parts_per_row]
   int max_prefix_chunks;  // per group
-  int max_resp_chunks;    // per sequence
+  int max_resp_chunks;    // per sequence (at the short chunk length)
+  int parts_per_row;      // max_prefix_chunks + max_resp_chunks
   int max_parts;          // capacity of part_o / part_lse
+  int max_prefix_items;   // capacity of prefix_items
+  int max_resp_items;     // capacity of resp_items
 };
 
 // Partial-result slot, kept inside the workspace even for a workspace that was
@@ -66,23 +84,10 @@ __device__ inline uint32_t pack_bf16x2(float lo, float hi) {
 }
 
 // ---- OCP e4m3fn -----------------------------------------------------------
-// Exact decode of two codes (bytes 0 and 1 of `w` when hi == false, bytes 2
-// and 3 otherwise) to fp32. Each code's 7 magnitude bits are placed as an
-// fp16 with exponent field e and mantissa m << 7, which equals the e4m3 value
-// times 2^-8 for normal and subnormal codes alike; the caller folds the 2^8
-// into its per-page scale. The NaN code (S.1111.111) is never produced by the
-// append path and decodes to 480 here.
-__device__ inline void e4m3x2_to_f32_scaled(uint32_t w, bool hi, float& a, float& b) {
-  uint32_t x = hi ? (w >> 16) : w;  // codes in bits 0..7 and 8..15
-  // Spread byte 1 into bits 16..23: x' = b0 | b1 << 16.
-  uint32_t sp = (x & 0xFFu) | ((x & 0xFF00u) << 8);
-  uint32_t h = ((sp & 0x00800080u) << 8) | ((sp & 0x007F007Fu) << 7);
-  typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
-  f16x2_t hv = __builtin_bit_cast(f16x2_t, h);
-  a = (float)hv[0];
-  b = (float)hv[1];
+// Decoding uses gfx950's conversion instructions, which implement OCP e4m3fn.
+__device__ inline float e4m3_to_f32(uint32_t code) {
+  return __builtin_amdgcn_cvt_f32_fp8((int)code, 0);
 }
-constexpr float kE4m3DecodeScale = 256.0f;  // undoes the 2^-8 of e4m3x2_to_f32_scaled
 
 // fp32 -> e4m3fn code, round to nearest even, saturating at +-448.
 __device__ inline uint32_t f32_to_e4m3(float x) {

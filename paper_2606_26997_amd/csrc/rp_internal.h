@@ -19,19 +19,25 @@ __host__ __device__ inline int prefix_chunks(int P, int max_prefix_pages, int ma
   const int n = cdiv(cdiv(clamp_len(P, max_prefix_pages), kPage), kPrefixChunkPages);
   return n > max_chunks ? max_chunks : n;
 }
-__host__ __device__ inline int resp_chunks(int L, int max_resp_pages, int max_chunks) {
-  const int n = cdiv(cdiv(clamp_len(L, max_resp_pages), kPage), kRespChunkPages);
+__host__ __device__ inline int resp_chunks(int L, int max_resp_pages, int max_chunks, int chunk_pages) {
+  const int n = cdiv(cdiv(clamp_len(L, max_resp_pages), kPage), chunk_pages);
   return n > max_chunks ? max_chunks : n;
+}
+// The planner's response chunk length, read back on the device.
+__device__ inline int planned_chunk_pages(const int* hdr) {
+  const int c = hdr[kHdrRespChunkPages];
+  return c == kRespChunkPagesMax ? kRespChunkPagesMax : kRespChunkPagesMin;
 }
 __device__ inline int clamp_page(int p, int num_pages) {
   return (unsigned)p < (unsigned)num_pages ? p : 0;
 }
 
 struct PlanArgs {
-  int num_seqs, num_groups, num_q_heads;
+  int num_seqs, num_groups, num_q_heads, num_pages;
   const int* seq_to_group;
   const int* prefix_lens;
   const int* resp_lens;
+  const int* resp_block_table;
   int max_prefix_pages, max_resp_pages;
   PlanView view;
 };
@@ -55,13 +61,22 @@ struct AttnArgs {
   PlanView view;
 };
 
+// Combine input: either an explicit CSR (row_offs != null) or the planned
+// fixed slots, whose part counts follow from the lengths.
 struct CombineArgs {
   const float* o_parts;
   const float* lse_parts;
-  const int* row_offs;
+  const int* row_offs;   // CSR [num_rows + 1], or null for planned slots
   int num_rows;
-  void* out;         // bf16 [rows][D]
-  float* lse;        // [rows] or null
+  void* out;             // bf16 [rows][D]
+  float* lse;            // [rows] or null
+  // planned slots only
+  const int* plan_hdr;
+  int num_q_heads, num_groups, parts_per_row, max_prefix_pages, max_resp_pages;
+  int max_prefix_chunks, max_resp_chunks;
+  const int* seq_to_group;
+  const int* prefix_lens;
+  const int* resp_lens;
 };
 
 struct AppendArgs {
@@ -90,11 +105,9 @@ struct ValidateArgs {
 };
 
 hipError_t launch_plan(const PlanArgs& a, hipStream_t stream);
-// grid sizes are upper bounds from host scalars; idle waves exit at once.
-hipError_t launch_prefix_parts(const AttnArgs& a, int head_dim, int n_rep, bool fp8,
-                               long long max_items, hipStream_t stream);
-hipError_t launch_resp_parts(const AttnArgs& a, int head_dim, int n_rep, bool fp8,
-                             long long max_items, hipStream_t stream);
+// Grid sizes are upper bounds from host scalars; idle waves exit at once.
+hipError_t launch_attn_parts(const AttnArgs& a, int head_dim, int n_rep, bool fp8, long long max_prefix_items,
+                             long long max_resp_items, hipStream_t stream);
 hipError_t launch_combine(const CombineArgs& a, int head_dim, hipStream_t stream);
 hipError_t launch_append(const AppendArgs& a, int head_dim, bool fp8, hipStream_t stream);
 hipError_t launch_validate(const ValidateArgs& a, hipStream_t stream);
