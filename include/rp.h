@@ -155,8 +155,12 @@ rp_status rp_lse_combine(const float* o_parts, const float* lse_parts,
  * A decode step's layout is shared by every layer, so a caller can plan once
  * and run the attention of all layers against the same plan. */
 
-/* Build the work plan (group member lists, prefix work items, response work
- * items ordered longest first) in `workspace` from the layout's device arrays.
+/* Build the work plan in `workspace` from the layout's device arrays: group
+ * member lists, prefix work items (16-page chunks of each live group's
+ * prefix), response work items (every response cut into pieces of B pages,
+ * B = 32 or 64 chosen per batch from the average response length, the
+ * B-page pieces first and then each response's shorter last piece by
+ * decreasing size), and the number of partial results per query row.
  * Must be re-run whenever seq_to_group, prefix_lens or resp_lens change.
  * Supports num_groups <= 4096. */
 rp_status rp_plan(const rp_paged_kv* kv, const rp_group_layout* layout,
@@ -165,7 +169,8 @@ rp_status rp_plan(const rp_paged_kv* kv, const rp_group_layout* layout,
 /* All partial results for a planned workspace, in one kernel launch:
  * group-prefix parts (each group's prompt prefix read once per kv-head and
  * applied to all query rows of its live members on the matrix cores) and
- * response parts (each sequence's own response pages in fixed page chunks).
+ * response parts (each sequence's own response pages, one planned piece per
+ * unit).
  * q and softmax_scale as in rp_group_decode_attn. */
 rp_status rp_attn_parts(const rp_paged_kv* kv, const rp_group_layout* layout,
                         const void* q, float softmax_scale,
@@ -176,6 +181,27 @@ rp_status rp_attn_parts(const rp_paged_kv* kv, const rp_group_layout* layout,
 rp_status rp_combine_parts(const rp_paged_kv* kv, const rp_group_layout* layout,
                            void* out, float* lse,
                            void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Where rp_plan stores its results inside a workspace, for tests and tools
+ * that read a plan back (host-side only; launches nothing). Offsets are in
+ * bytes from the workspace start. Contents, all int32:
+ *   hdr[16]: [0] prefix items, [1] response items, [2] of those, the B-page
+ *            pieces (they come first), [3] B, the piece length in pages;
+ *   grp_off[G + 1], grp_members[S]: CSR of each group's live sequences;
+ *   prefix_items: (group, chunk of 16 prefix pages) pairs;
+ *   resp_items: (sequence, first page index in the sequence's block table,
+ *               tokens, partial-result slot) quadruples, in dispatch order;
+ *   resp_first_page: the physical page id of each response item's first page;
+ *   seq_parts[S]: partial results per query row of each sequence.
+ * part_o (fp32 [max_parts][head_dim]) and part_lse (fp32 [max_parts]) hold
+ * the partial results of query row r in slots r * parts_per_row + k. */
+typedef struct {
+  size_t hdr, grp_off, grp_members, prefix_items, resp_items, resp_first_page, seq_parts;
+  size_t part_o, part_lse;
+  int32_t max_prefix_items, max_resp_items, parts_per_row, max_parts;
+} rp_plan_info;
+
+rp_status rp_plan_layout(const rp_paged_kv* kv, const rp_group_layout* layout, rp_plan_info* info);
 
 /* Check the layout's device arrays against the pool and table sizes: groups
  * in range, lengths non-negative and within the table widths, every page id

@@ -27,7 +27,7 @@ RP_KV_FP8_E4M3 = 1
 
 EXPORTED = ("rp_status_string", "rp_last_error", "rp_kv_append",
             "rp_group_decode_attn_workspace_size", "rp_group_decode_attn", "rp_lse_combine",
-            "rp_plan", "rp_attn_parts", "rp_combine_parts", "rp_validate_layout")
+            "rp_plan", "rp_attn_parts", "rp_combine_parts", "rp_plan_layout", "rp_validate_layout")
 
 
 class RpPagedKV(ctypes.Structure):
@@ -45,6 +45,12 @@ class RpGroupLayout(ctypes.Structure):
                 ("prefix_block_table", ctypes.c_void_p), ("max_prefix_pages", ctypes.c_int32),
                 ("resp_lens", ctypes.c_void_p), ("resp_block_table", ctypes.c_void_p),
                 ("max_resp_pages", ctypes.c_int32)]
+
+
+class RpPlanInfo(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_size_t) for n in ("hdr", "grp_off", "grp_members", "prefix_items", "resp_items",
+                                                 "resp_first_page", "seq_parts", "part_o", "part_lse")] + \
+               [(n, ctypes.c_int32) for n in ("max_prefix_items", "max_resp_items", "parts_per_row", "max_parts")]
 
 
 class RpError(RuntimeError):
@@ -75,6 +81,7 @@ def load() -> ctypes.CDLL:
         "rp_plan": (ctypes.c_int, [P, P, P, ctypes.c_size_t, P]),
         "rp_attn_parts": (ctypes.c_int, [P, P, P, F32, P, ctypes.c_size_t, P]),
         "rp_combine_parts": (ctypes.c_int, [P, P, P, P, P, ctypes.c_size_t, P]),
+        "rp_plan_layout": (ctypes.c_int, [P, P, P]),
         "rp_validate_layout": (ctypes.c_int, [P, P, P]),
     }
     for name, (res, args) in sig.items():
@@ -185,6 +192,12 @@ def lse_combine(o_parts, lse_parts, row_part_offsets, num_rows, head_dim, out, l
     _check(load().rp_lse_combine(_ptr(o_parts), _ptr(lse_parts), _ptr(row_part_offsets),
                                  int(num_rows), int(head_dim), _ptr(out), _ptr(lse_out),
                                  _stream(stream)), "rp_lse_combine")
+
+
+def plan_layout(kv, layout) -> RpPlanInfo:
+    info = RpPlanInfo()
+    _check(load().rp_plan_layout(ctypes.byref(kv), ctypes.byref(layout), ctypes.byref(info)), "rp_plan_layout")
+    return info
 
 
 def validate_layout(kv, layout, stream=None) -> None:

@@ -105,5 +105,22 @@ class DeviceBatch:
     def combine_parts(self, stream=None):
         B.combine_parts(self.kv, self.attn_layout, self.out, self.lse, self.workspace, stream)
 
+    def plan_contents(self):
+        """The planned workspace read back to the host (numpy int32 arrays)."""
+        info = B.plan_layout(self.kv, self.attn_layout)
+        torch.cuda.synchronize()
+        ws = self.workspace.cpu().numpy()
+        S, G = self.seq_to_group.shape[0], self.prefix_lens.shape[0]
+
+        def arr(off, count, width=1):
+            return ws[off:off + 4 * count * width].view(np.int32).reshape(-1, width) if width > 1 else \
+                ws[off:off + 4 * count].view(np.int32)
+        hdr = arr(info.hdr, 16)
+        return dict(hdr=hdr, grp_off=arr(info.grp_off, G + 1), grp_members=arr(info.grp_members, S),
+                    prefix_items=arr(info.prefix_items, int(hdr[0]), 2),
+                    resp_items=arr(info.resp_items, int(hdr[1]), 4),
+                    resp_first_page=arr(info.resp_first_page, int(hdr[1])),
+                    seq_parts=arr(info.seq_parts, S), parts_per_row=info.parts_per_row)
+
     def validate(self, stream=None):
         B.validate_layout(self.kv, self.attn_layout, stream)

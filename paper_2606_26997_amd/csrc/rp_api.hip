@@ -100,7 +100,7 @@ rp_status check_shape(const rp_paged_kv* kv, const rp_group_layout* l, Shape* sh
 
 // Workspace layout, 256-byte aligned sections.
 struct WsLayout {
-  size_t hdr, grp_off, members, pitems, ritems, rpage0, part_o, part_lse, total;
+  size_t hdr, grp_off, members, pitems, ritems, rpage0, seq_parts, part_o, part_lse, total;
   long long max_pitems, max_ritems, max_parts;
   int max_pc, max_rc;
 };
@@ -124,6 +124,7 @@ bool ws_layout(const Shape& sh, WsLayout* w) {
   w->pitems = o;    o = align_up(o + sizeof(int2) * (size_t)w->max_pitems);
   w->ritems = o;    o = align_up(o + sizeof(int4) * (size_t)w->max_ritems);
   w->rpage0 = o;    o = align_up(o + sizeof(int) * (size_t)w->max_ritems);
+  w->seq_parts = o; o = align_up(o + sizeof(int) * (size_t)sh.S);
   w->part_o = o;    o = align_up(o + sizeof(float) * (size_t)w->max_parts * sh.D);
   w->part_lse = o;  o = align_up(o + sizeof(float) * (size_t)w->max_parts);
   w->total = o;
@@ -139,6 +140,7 @@ rp::PlanView plan_view(void* ws, const WsLayout& w) {
   v.prefix_items = reinterpret_cast<int2*>(b + w.pitems);
   v.resp_items = reinterpret_cast<int4*>(b + w.ritems);
   v.resp_first_page = reinterpret_cast<int*>(b + w.rpage0);
+  v.seq_parts = reinterpret_cast<int*>(b + w.seq_parts);
   v.part_o = reinterpret_cast<float*>(b + w.part_o);
   v.part_lse = reinterpret_cast<float*>(b + w.part_lse);
   v.max_prefix_chunks = w.max_pc;
@@ -272,17 +274,9 @@ rp_status rp_combine_parts(const rp_paged_kv* kv, const rp_group_layout* l, void
   c.num_rows = sh.S * sh.Hq;
   c.out = out;
   c.lse = lse;
-  c.plan_hdr = v.hdr;
+  c.seq_parts = v.seq_parts;
   c.num_q_heads = sh.Hq;
-  c.num_groups = sh.G;
   c.parts_per_row = v.parts_per_row;
-  c.max_prefix_pages = sh.max_pp;
-  c.max_resp_pages = sh.max_rp;
-  c.max_prefix_chunks = v.max_prefix_chunks;
-  c.max_resp_chunks = v.max_resp_chunks;
-  c.seq_to_group = l->seq_to_group;
-  c.prefix_lens = l->prefix_lens;
-  c.resp_lens = l->resp_lens;
   hipError_t e = rp::launch_combine(c, sh.D, stream);
   return e == hipSuccess ? RP_OK : hip_fail(e, "combine kernel launch");
 }
@@ -353,6 +347,30 @@ rp_status rp_kv_append(const rp_paged_kv* kv, const rp_group_layout* l, const vo
   a.v_new = v_new;
   hipError_t e = rp::launch_append(a, sh.D, sh.fp8, stream);
   return e == hipSuccess ? RP_OK : hip_fail(e, "append kernel launch");
+}
+
+rp_status rp_plan_layout(const rp_paged_kv* kv, const rp_group_layout* l, rp_plan_info* info) {
+  g_err[0] = 0;
+  if (info == nullptr) return fail(RP_ERR_INVALID_ARG, "info is NULL");
+  Shape sh;
+  rp_status st = check_shape(kv, l, &sh);
+  if (st != RP_OK) return st;
+  WsLayout w;
+  if (!ws_layout(sh, &w)) return fail(RP_ERR_UNSUPPORTED, "layout too large for the work plan");
+  info->hdr = w.hdr;
+  info->grp_off = w.grp_off;
+  info->grp_members = w.members;
+  info->prefix_items = w.pitems;
+  info->resp_items = w.ritems;
+  info->resp_first_page = w.rpage0;
+  info->seq_parts = w.seq_parts;
+  info->part_o = w.part_o;
+  info->part_lse = w.part_lse;
+  info->max_prefix_items = (int32_t)w.max_pitems;
+  info->max_resp_items = (int32_t)w.max_ritems;
+  info->parts_per_row = w.max_pc + w.max_rc;
+  info->max_parts = (int32_t)w.max_parts;
+  return RP_OK;
 }
 
 rp_status rp_validate_layout(const rp_paged_kv* kv, const rp_group_layout* l, hipStream_t stream) {

@@ -19,8 +19,8 @@
 // DPP, every group of LPT lanes keeps its own online-softmax state, and the
 // states are merged once per unit. Page loads are software-pipelined: the next
 // page's K is requested as soon as this page's scores exist and its V as soon as
-// this page's V is unpacked. The response chunk length (pages per unit) is
-// chosen by the planner for the batch.
+// this page's V is unpacked. How responses split into items is the planner's
+// choice for the batch.
 //
 // Each unit writes one partial (o normalised, lse natural-log) per query row
 // into its fixed slot (row, chunk); the combine kernel merges a row's parts.
@@ -291,14 +291,13 @@ __device__ void resp_unit(const AttnArgs& a, int item, int h) {
   const char* kpool = static_cast<const char*>(a.k_pages);
   const char* vpool = static_cast<const char*>(a.v_pages);
 
-  // The item record and its first page id come straight from the plan, so the
-  // first K/V loads depend on one load only.
+  // The item record (sequence, first page, tokens, slot) and its first page id
+  // come straight from the plan, so the first K/V loads depend on one load only.
   const int4 m = a.view.resp_items[item];
   const int s = min(max(m.x, 0), a.num_seqs - 1);
-  const int chunk = planned_chunk_pages(a.view.hdr);
-  const int c = min(max(m.y, 0), a.view.max_resp_chunks - 1);
-  const int npc = m.w;
-  const int ntok = min(chunk * kPage, min(m.z, a.max_resp_pages * kPage) - c * (chunk * kPage));
+  const int p0 = min(max(m.y, 0), a.max_resp_pages);
+  const int ntok = min(max(m.z, 0), min(kRespChunkPagesMax, a.max_resp_pages - p0) * kPage);
+  const int slot = min(max(m.w, 0), a.view.parts_per_row - 1);
   const int npages = cdiv(ntok, kPage);
   int page = clamp_page(a.view.resp_first_page[item], a.num_pages);
   uint4 kr[LOADS], vr[LOADS];
@@ -309,7 +308,7 @@ __device__ void resp_unit(const AttnArgs& a, int item, int h) {
 #pragma unroll
     for (int i = 0; i < LOADS; ++i) vr[i] = *reinterpret_cast<const uint4*>(vpool + blk + i * 1024);
   }
-  const int* bt = a.resp_block_table + (size_t)s * a.max_resp_pages + c * chunk;
+  const int* bt = a.resp_block_table + (size_t)s * a.max_resp_pages + p0;
 
   // This lane's EPL head_dim elements of the NREP query rows of kv-head h (bf16).
   const uint16_t* qrow =
@@ -416,7 +415,7 @@ __device__ void resp_unit(const AttnArgs& a, int item, int h) {
     float oo[EPL];
 #pragma unroll
     for (int e = 0; e < EPL; ++e) oo[e] = xor_sum_from<LPT>(o[r][e] * w) * inv;
-    const int part = clamp_part((row0 + r) * a.view.parts_per_row + npc + c, a.view.max_parts);
+    const int part = clamp_part((row0 + r) * a.view.parts_per_row + slot, a.view.max_parts);
     if (tg == 0) {
       float4* dst = reinterpret_cast<float4*>(a.view.part_o + (size_t)part * D + sub * EPL);
 #pragma unroll
@@ -427,32 +426,39 @@ __device__ void resp_unit(const AttnArgs& a, int item, int h) {
 }
 
 // All partial results in one launch, one unit per one-wave block: the first
-// `prefix_blocks` blocks take group-prefix units (dispatched first, so their
-// short, latency-bound MFMA work overlaps the streaming response units), the
-// rest take response units in plan order (longest first). Blocks beyond the
-// planned counts exit at once. The item counts are clamped to the plan's
-// capacity, so even a workspace that was never planned cannot send a wave
-// outside the item lists.
+// blocks take the group-prefix units (dispatched first; their short,
+// latency-bound MFMA work overlaps the response units that fill the rest of
+// the GPU), the following blocks the response units in plan order (big items
+// first, then small ones by decreasing size), and blocks beyond the planned
+// counts exit at once. Units are not interleaved by block id: workgroups are
+// dealt round-robin to XCDs and then to shader engines, and any periodic
+// pattern of unit kinds would correlate with that and unbalance them. The
+// counts are clamped to the plan's capacity, so even a workspace that was
+// never planned cannot send a wave outside the item lists.
 template <int D, int NREP, bool FP8>
-__global__ __launch_bounds__(64) void attn_parts_kernel(const AttnArgs a, int prefix_blocks) {
+__global__ __launch_bounds__(64) void attn_parts_kernel(const AttnArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t vt[kPage * (D + 4)];
   const int Hkv = a.num_kv_heads;
-  int b = blockIdx.x;
-  if (b < prefix_blocks) {
+  const int n_pre = min(max(a.view.hdr[kHdrPrefixItems], 0), a.view.max_prefix_items) * Hkv;
+  const int n_resp = min(max(a.view.hdr[kHdrRespItems], 0), a.view.max_resp_items) * Hkv;
+  const int b = blockIdx.x;
+  if (b < n_pre) {
     const int item = b / Hkv;
-    if (item < min(a.view.hdr[kHdrPrefixItems], a.view.max_prefix_items))
-      prefix_unit<D, NREP, FP8>(a, item, b - item * Hkv, vt);
+    prefix_unit<D, NREP, FP8>(a, item, b - item * Hkv, vt);
     return;
   }
-  b -= prefix_blocks;
-  const int item = b / Hkv;
-  if (item < min(a.view.hdr[kHdrRespItems], a.view.max_resp_items)) resp_unit<D, NREP, FP8>(a, item, b - item * Hkv);
+  const int resp = b - n_pre;
+  if (resp < n_resp) {
+    const int item = resp / Hkv;
+    resp_unit<D, NREP, FP8>(a, item, resp - item * Hkv);
+  }
 }
 
+// Grid: one block per unit of the largest plan that fits the workspace.
 template <int D, int NREP, bool FP8>
 hipError_t launch_one(const AttnArgs& a, long long prefix_blocks, long long resp_blocks, hipStream_t st) {
-  attn_parts_kernel<D, NREP, FP8>
-      <<<dim3((unsigned)(prefix_blocks + resp_blocks)), dim3(64), 0, st>>>(a, (int)prefix_blocks);
+  const long long blocks = prefix_blocks + resp_blocks;
+  attn_parts_kernel<D, NREP, FP8><<<dim3((unsigned)blocks), dim3(64), 0, st>>>(a);
   return hipGetLastError();
 }
 

@@ -3,7 +3,8 @@
 // Parts with lse_i = -inf are empty and their o_i is never added. A row's
 // parts are read in batches: LPP lanes cover one part's head_dim with float4
 // loads, so one load instruction fetches 64 / LPP parts and a batch keeps
-// kBatch such loads in flight per wave.
+// kBatch such loads in flight per wave. The first batch's partial outputs are
+// requested together with their lse values, before the row maximum is known.
 #include "rp_device.h"
 #include "rp_internal.h"
 
@@ -12,6 +13,35 @@ namespace {
 
 constexpr int kCombineWaves = 4;
 constexpr int kBatch = 8;
+
+template <int D>
+__device__ inline void load_batch(const CombineArgs& a, int p0, int n, int base, int slot, int sub, float* lp,
+                                  float4* ov) {
+  constexpr int PPI = 64 / (D / 4);
+#pragma unroll
+  for (int b = 0; b < kBatch; ++b) {
+    const int k = base + b * PPI + slot;
+    lp[b] = -INFINITY;
+    ov[b] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (k < n) {
+      lp[b] = a.lse_parts[p0 + k];
+      ov[b] = *reinterpret_cast<const float4*>(a.o_parts + (size_t)(p0 + k) * D + sub * 4);
+    }
+  }
+}
+
+__device__ inline void add_batch(const float* lp, const float4* ov, float mx, float4& acc, float& wsum) {
+#pragma unroll
+  for (int b = 0; b < kBatch; ++b) {
+    const bool live = lp[b] != -INFINITY;
+    const float w = live ? fast_exp2((lp[b] - mx) * kLog2e) : 0.f;
+    wsum += w;
+    acc.x = live ? fmaf(w, ov[b].x, acc.x) : acc.x;
+    acc.y = live ? fmaf(w, ov[b].y, acc.y) : acc.y;
+    acc.z = live ? fmaf(w, ov[b].z, acc.z) : acc.z;
+    acc.w = live ? fmaf(w, ov[b].w, acc.w) : acc.w;
+  }
+}
 
 template <int D>
 __global__ __launch_bounds__(64 * kCombineWaves) void combine_kernel(const CombineArgs a) {
@@ -27,43 +57,26 @@ __global__ __launch_bounds__(64 * kCombineWaves) void combine_kernel(const Combi
     p0 = a.row_offs[row];
     n = a.row_offs[row + 1] - p0;
   } else {
-    const int s = row / a.num_q_heads;
-    const int g = clamp_group(a.seq_to_group[s], a.num_groups);
-    n = prefix_chunks(a.prefix_lens[g], a.max_prefix_pages, a.max_prefix_chunks) +
-        resp_chunks(a.resp_lens[s], a.max_resp_pages, a.max_resp_chunks, planned_chunk_pages(a.plan_hdr));
+    n = min(max(a.seq_parts[row / a.num_q_heads], 0), a.parts_per_row);
     p0 = row * a.parts_per_row;
   }
 
+  float lp[kBatch];
+  float4 ov[kBatch];
+  load_batch<D>(a, p0, n, 0, slot, sub, lp, ov);
   float mx = -INFINITY;
-  for (int i = lane; i < n; i += 64) mx = fmaxf(mx, a.lse_parts[p0 + i]);
+#pragma unroll
+  for (int b = 0; b < kBatch; ++b) mx = fmaxf(mx, lp[b]);
+  for (int i = PPI * kBatch + lane; i < n; i += 64) mx = fmaxf(mx, a.lse_parts[p0 + i]);
   mx = xor_max_from<1>(mx);
 
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
   float wsum = 0.f;
   if (mx != -INFINITY) {
-    for (int base = 0; base < n; base += PPI * kBatch) {
-      float lp[kBatch];
-      float4 ov[kBatch];
-#pragma unroll
-      for (int b = 0; b < kBatch; ++b) {
-        const int k = base + b * PPI + slot;
-        lp[b] = -INFINITY;
-        ov[b] = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (k < n) {
-          lp[b] = a.lse_parts[p0 + k];
-          ov[b] = *reinterpret_cast<const float4*>(a.o_parts + (size_t)(p0 + k) * D + sub * 4);
-        }
-      }
-#pragma unroll
-      for (int b = 0; b < kBatch; ++b) {
-        const bool live = lp[b] != -INFINITY;
-        const float w = live ? fast_exp2((lp[b] - mx) * kLog2e) : 0.f;
-        wsum += w;
-        acc.x = live ? fmaf(w, ov[b].x, acc.x) : acc.x;
-        acc.y = live ? fmaf(w, ov[b].y, acc.y) : acc.y;
-        acc.z = live ? fmaf(w, ov[b].z, acc.z) : acc.z;
-        acc.w = live ? fmaf(w, ov[b].w, acc.w) : acc.w;
-      }
+    add_batch(lp, ov, mx, acc, wsum);
+    for (int base = PPI * kBatch; base < n; base += PPI * kBatch) {
+      load_batch<D>(a, p0, n, base, slot, sub, lp, ov);
+      add_batch(lp, ov, mx, acc, wsum);
     }
   }
   acc.x = xor_sum_from<LPP>(acc.x);

@@ -9,13 +9,16 @@ namespace rp {
 
 // Tokens per KV page (the only page size the kernels are built for).
 constexpr int kPage = 16;
-// Pages per prefix work item, and the range of pages per response work item
-// (split-KV chunk). The planner picks the response chunk for each batch: the
-// short one when the average response is below kLongResponsePages pages, the
-// long one otherwise (longer chunks amortise each unit's start-up latency;
-// shorter ones keep the end of the launch balanced). Workspace is sized for
-// the short chunk.
-constexpr int kPrefixChunkPages = 4;
+// Pages per prefix work item, and the split of each response into work items:
+// a response of P pages becomes floor(P / B) pieces of B pages and, if P is
+// not a multiple of B, one ragged piece with the rest. Items are dispatched
+// largest first (all B-sized pieces, then the ragged ones by decreasing
+// size). The planner picks B per batch: kRespChunkPagesMin when the average
+// response is below kLongResponsePages pages, else kRespChunkPagesMax; large
+// pieces amortise each unit's start-up latency, and measured alternatives
+// with extra small pieces at the end cost more start-ups than they saved.
+// Workspace is sized for the smaller B.
+constexpr int kPrefixChunkPages = 16;
 constexpr int kRespChunkPagesMin = 32;
 constexpr int kRespChunkPagesMax = 64;
 constexpr int kLongResponsePages = 256;
@@ -27,7 +30,7 @@ constexpr float kLn2 = 0.6931471805599453f;
 enum : int {
   kHdrPrefixItems = 0,
   kHdrRespItems = 1,
-  kHdrFullRespItems = 2,
+  kHdrBigRespItems = 2,   // B-sized response items (they come first)
   kHdrRespChunkPages = 3,
   kHdrSlots = 16
 };
@@ -50,12 +53,13 @@ struct PlanView {
   int* grp_off;        // [G+1] CSR of members
   int* grp_members;    // [S]   members of each group in ascending order of arrival
   int2* prefix_items;  // [max_prefix_items]  (group, chunk)
-  int4* resp_items;    // [max_resp_items]    (sequence, chunk, clamped length, prefix chunks), longest first
+  int4* resp_items;    // [max_resp_items]    (sequence, first page, tokens, slot), longest first
   int* resp_first_page;  // [max_resp_items]  physical page of each response item's first page
+  int* seq_parts;      // [S] partial results per query row of each sequence
   float* part_o;       // [S*Hq*parts_per_row][D]
   float* part_lse;     // [S*Hq*parts_per_row]
   int max_prefix_chunks;  // per group
-  int max_resp_chunks;    // per sequence (at the short chunk length)
+  int max_resp_chunks;    // response items per sequence (at the smaller big-item length)
   int parts_per_row;      // max_prefix_chunks + max_resp_chunks
   int max_parts;          // capacity of part_o / part_lse
   int max_prefix_items;   // capacity of prefix_items

@@ -19,15 +19,6 @@ __host__ __device__ inline int prefix_chunks(int P, int max_prefix_pages, int ma
   const int n = cdiv(cdiv(clamp_len(P, max_prefix_pages), kPage), kPrefixChunkPages);
   return n > max_chunks ? max_chunks : n;
 }
-__host__ __device__ inline int resp_chunks(int L, int max_resp_pages, int max_chunks, int chunk_pages) {
-  const int n = cdiv(cdiv(clamp_len(L, max_resp_pages), kPage), chunk_pages);
-  return n > max_chunks ? max_chunks : n;
-}
-// The planner's response chunk length, read back on the device.
-__device__ inline int planned_chunk_pages(const int* hdr) {
-  const int c = hdr[kHdrRespChunkPages];
-  return c == kRespChunkPagesMax ? kRespChunkPagesMax : kRespChunkPagesMin;
-}
 __device__ inline int clamp_page(int p, int num_pages) {
   return (unsigned)p < (unsigned)num_pages ? p : 0;
 }
@@ -70,13 +61,9 @@ struct CombineArgs {
   int num_rows;
   void* out;             // bf16 [rows][D]
   float* lse;            // [rows] or null
-  // planned slots only
-  const int* plan_hdr;
-  int num_q_heads, num_groups, parts_per_row, max_prefix_pages, max_resp_pages;
-  int max_prefix_chunks, max_resp_chunks;
-  const int* seq_to_group;
-  const int* prefix_lens;
-  const int* resp_lens;
+  // planned slots only: parts per query row of each sequence, from the plan
+  const int* seq_parts;
+  int num_q_heads, parts_per_row;
 };
 
 struct AppendArgs {

@@ -2,12 +2,11 @@
 //  * per-group member lists (CSR over sequences),
 //  * prefix work items (group, chunk of kPrefixChunkPages prefix pages) for
 //    groups with at least one live member,
-//  * the response chunk length for this batch (short or long, from the
-//    average response length),
-//  * response work items (sequence, chunk, clamped response length, prefix
-//    chunks of the sequence's group) with the physical id of each item's first
-//    page, ordered longest first: every full chunk, then the ragged last chunks
-//    by decreasing page count, so the last free slots get the least work.
+//  * the piece length B for this batch (from the average response length),
+//  * the number of partial results per query row of each sequence,
+//  * response work items (sequence, first page, tokens, partial-result slot)
+//    with the physical id of each item's first page: every B-page piece
+//    first, then the ragged last pieces by decreasing size.
 // Group counters live in LDS; scans are wavefront scans plus one pass over
 // the wave totals.
 #include "rp_device.h"
@@ -47,46 +46,95 @@ __device__ long long block_excl_scan(long long v, long long* s_tot, long long& t
   return base + incl - v;
 }
 
+// Sum over the 64 lanes of a wave (every lane gets the total).
+__device__ inline long long wave_sum(long long v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
 __device__ inline long long pack2(int hi, int lo) { return ((long long)hi << 32) + (long long)(unsigned)lo; }
 __device__ inline int hi32(long long v) { return (int)(v >> 32); }
 __device__ inline int lo32(long long v) { return (int)(v & 0xFFFFFFFFll); }
 
+// Sequences planned per pass: their group ids, lengths and piece offsets stay
+// in LDS (a batch with more sequences takes several passes).
+constexpr int kPlanSeqBlock = 4096;
+constexpr int kSeqPerThread = kPlanSeqBlock / kPlanThreads;
+// B-sized pieces written per thread per round; their block-table loads are
+// issued together with those of the thread's ragged pieces.
+constexpr int kItemBatch = 8;
+constexpr int kRoundItems = kItemBatch * kPlanThreads;
+
 __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
-  __shared__ int s_cnt[kPlanMaxGroups];
-  __shared__ int s_fill[kPlanMaxGroups];
-  __shared__ int s_hist[kRespChunkPagesMax];   // ragged chunks per page count
-  __shared__ int s_hoff[kRespChunkPagesMax];
+  __shared__ int s_cnt[kPlanMaxGroups];   // members per group, then the group's next member slot
+  __shared__ int s_gpc[kPlanMaxGroups];   // prefix chunks per group
+  __shared__ int s_sg[kPlanSeqBlock];     // clamped group of each sequence of the pass
+  __shared__ int s_sl[kPlanSeqBlock];     // clamped response length of each sequence of the pass
+  __shared__ int s_off[kPlanSeqBlock];    // first B-sized piece of each sequence of the pass
+  __shared__ int s_own[kRoundItems];      // sequence (of the pass) of each B-sized piece of a round
+  __shared__ int s_hist[2][kRespChunkPagesMax];  // ragged pieces per page count, for B = min and max
+  __shared__ int s_hoff[kRespChunkPagesMax];     // next item index per ragged page count
+  __shared__ int s_nbig[2];                      // B-sized pieces, for B = min and max
   __shared__ long long s_tot[kPlanWaves];
   __shared__ unsigned long long s_pages;
-  __shared__ int s_off[kPlanThreads];   // per-thread item offsets of one chunk of sequences
-  __shared__ int s_len[kPlanThreads];
-  __shared__ int s_npc[kPlanThreads];
-  const int t = threadIdx.x;
+  const int t = threadIdx.x, lane = t & 63;
   const int S = a.num_seqs, G = a.num_groups;
   const PlanView v = a.view;
   const int* bt = a.resp_block_table;
 
-  for (int g = t; g < G; g += kPlanThreads) {
-    s_cnt[g] = 0;
-    s_fill[g] = 0;
-  }
-  if (t < kRespChunkPagesMax) s_hist[t] = 0;
+  for (int g = t; g < G; g += kPlanThreads) s_cnt[g] = 0;
+  if (t < 2 * kRespChunkPagesMax) s_hist[t / kRespChunkPagesMax][t % kRespChunkPagesMax] = 0;
+  if (t < 2) s_nbig[t] = 0;
   if (t == 0) s_pages = 0;
   __syncthreads();
 
-  // Live members per group and the total number of response pages.
+  // One pass over the inputs: group sizes, prefix chunks per group, total
+  // response pages, and the piece counts for both piece lengths.
+  for (int g = t; g < G; g += kPlanThreads)
+    s_gpc[g] = prefix_chunks(a.prefix_lens[g], a.max_prefix_pages, v.max_prefix_chunks);
   unsigned long long my_pages = 0;
+  int my_big[2] = {0, 0};
   for (int s = t; s < S; s += kPlanThreads) {
-    atomicAdd(&s_cnt[clamp_group(a.seq_to_group[s], G)], 1);
-    my_pages += cdiv(clamp_len(a.resp_lens[s], a.max_resp_pages), kPage);
+    const int g = clamp_group(a.seq_to_group[s], G);
+    const int L = clamp_len(a.resp_lens[s], a.max_resp_pages);
+    if (s < kPlanSeqBlock) {
+      s_sg[s] = g;
+      s_sl[s] = L;
+    }
+    atomicAdd(&s_cnt[g], 1);
+    const int pages = cdiv(L, kPage);
+    my_pages += pages;
+    my_big[0] += pages / kRespChunkPagesMin;
+    my_big[1] += pages / kRespChunkPagesMax;
+    if (pages % kRespChunkPagesMin) atomicAdd(&s_hist[0][pages % kRespChunkPagesMin], 1);
+    if (pages % kRespChunkPagesMax) atomicAdd(&s_hist[1][pages % kRespChunkPagesMax], 1);
   }
-  atomicAdd(&s_pages, my_pages);
+  // One LDS atomic per wave: same-address atomics from every thread serialise.
+  my_pages = (unsigned long long)wave_sum((long long)my_pages);
+  const long long big = wave_sum(pack2(my_big[0], my_big[1]));
+  if (lane == 0) {
+    atomicAdd(&s_pages, my_pages);
+    atomicAdd(&s_nbig[0], hi32(big));
+    atomicAdd(&s_nbig[1], lo32(big));
+  }
   __syncthreads();
-  const int chunk =
-      s_pages >= (unsigned long long)S * kLongResponsePages ? kRespChunkPagesMax : kRespChunkPagesMin;
-  for (int s = t; s < S; s += kPlanThreads) {
-    const int rem = cdiv(clamp_len(a.resp_lens[s], a.max_resp_pages), kPage) % chunk;
-    if (rem != 0) atomicAdd(&s_hist[rem], 1);
+  const int lc = s_pages >= (unsigned long long)S * kLongResponsePages ? 1 : 0;
+  const int chunk = lc ? kRespChunkPagesMax : kRespChunkPagesMin;
+  const int nbig = s_nbig[lc];
+
+  // Item order: every B-sized piece first, then the ragged pieces by
+  // decreasing page count (one wave scans the count bins, largest first).
+  if (t < 64) {
+    const int r = chunk - 1 - lane;
+    const int h = r >= 1 ? s_hist[lc][r] : 0;
+    const int incl = (int)wave_incl_scan(h, lane);
+    if (r >= 1) s_hoff[r] = nbig + incl - h;
+    if (lane == 63) {
+      v.hdr[kHdrRespItems] = nbig + incl;
+      v.hdr[kHdrBigRespItems] = nbig;
+      v.hdr[kHdrRespChunkPages] = chunk;
+    }
   }
 
   // Groups: member offsets and prefix items.
@@ -96,14 +144,14 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
     int cnt = 0, npc = 0;
     if (g < G) {
       cnt = s_cnt[g];
-      npc = cnt > 0 ? prefix_chunks(a.prefix_lens[g], a.max_prefix_pages, v.max_prefix_chunks) : 0;
+      npc = cnt > 0 ? s_gpc[g] : 0;
     }
     long long tot;
     const long long ex = block_excl_scan(pack2(cnt, npc), s_tot, tot);
     if (g < G) {
       const int off = carry_m + hi32(ex);
       v.grp_off[g] = off;
-      s_cnt[g] = off;  // from here on: the group's first member slot
+      s_cnt[g] = off;  // from here on: the group's next free member slot
       const int i0 = carry_i + lo32(ex);
       for (int c = 0; c < npc; ++c) v.prefix_items[i0 + c] = make_int2(g, c);
     }
@@ -113,69 +161,93 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
   if (t == 0) {
     v.grp_off[G] = carry_m;
     v.hdr[kHdrPrefixItems] = carry_i;
-    v.hdr[kHdrRespChunkPages] = chunk;
   }
-  __syncthreads();
+  __syncthreads();  // member cursors and ragged-piece cursors are complete
 
-  // Sequences: member placement and full response chunks. The items of each
-  // chunk of sequences are written by all threads together; item k belongs to
-  // the last sequence whose offset is <= k.
+  // Sequences, kPlanSeqBlock per pass: member slots and response items. A
+  // sequence's B-sized pieces take items in sequence order after those of the
+  // sequences before it; its ragged piece takes the next item of its page
+  // count.
   int carry_f = 0;
-  for (int base = 0; base < S; base += kPlanThreads) {
-    const int s = base + t;
-    int nfull = 0, L = 0, npc = 0;
-    if (s < S) {
-      const int g = clamp_group(a.seq_to_group[s], G);
-      v.grp_members[s_cnt[g] + atomicAdd(&s_fill[g], 1)] = s;
-      L = clamp_len(a.resp_lens[s], a.max_resp_pages);
-      npc = prefix_chunks(a.prefix_lens[g], a.max_prefix_pages, v.max_prefix_chunks);
-      nfull = cdiv(L, kPage) / chunk;
+  for (int base = 0; base < S; base += kPlanSeqBlock) {
+    const int n = min(S - base, kPlanSeqBlock);
+    if (base > 0) {
+      __syncthreads();  // the previous pass is done with the LDS copies
+      for (int k = t; k < n; k += kPlanThreads) {
+        s_sg[k] = clamp_group(a.seq_to_group[base + k], G);
+        s_sl[k] = clamp_len(a.resp_lens[base + k], a.max_resp_pages);
+      }
+      __syncthreads();
+    }
+    int cnt[kSeqPerThread], sum = 0;
+#pragma unroll
+    for (int j = 0; j < kSeqPerThread; ++j) {
+      const int k = t * kSeqPerThread + j;
+      cnt[j] = k < n ? cdiv(s_sl[k], kPage) / chunk : 0;
+      sum += cnt[j];
     }
     long long tot;
-    const int ex = (int)block_excl_scan(nfull, s_tot, tot);
-    s_off[t] = ex;
-    s_len[t] = L;
-    s_npc[t] = npc;
-    __syncthreads();
-    for (int k = t; k < (int)tot; k += kPlanThreads) {
-      int lo = 0, hi = kPlanThreads - 1;  // largest j with s_off[j] <= k
-      while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if (s_off[mid] <= k) lo = mid;
-        else hi = mid - 1;
-      }
-      const int sj = base + lo, c = k - s_off[lo];
-      const int item = carry_f + k;
-      v.resp_items[item] = make_int4(sj, c, s_len[lo], s_npc[lo]);
-      v.resp_first_page[item] = bt[(size_t)sj * a.max_resp_pages + c * chunk];
+    int off = (int)block_excl_scan(sum, s_tot, tot);
+#pragma unroll
+    for (int j = 0; j < kSeqPerThread; ++j) {
+      const int k = t * kSeqPerThread + j;
+      if (k < n) s_off[k] = off;
+      off += cnt[j];
     }
     __syncthreads();
-    carry_f += (int)tot;
-  }
 
-  // Ragged last chunks after all full ones, largest first.
-  if (t == 0) {
-    int off = carry_f;
-    for (int r = chunk - 1; r >= 1; --r) {
-      s_hoff[r] = off;
-      off += s_hist[r];
+    // Rounds of kRoundItems B-sized pieces: the owner of every piece of the
+    // round goes into LDS first, then thread t writes pieces t + u *
+    // kPlanThreads of the round, plus the member slot and ragged piece of
+    // sequences t + round * kPlanThreads, all block-table loads in one batch.
+    const int rounds = max(cdiv(n, kPlanThreads), cdiv((int)tot, kRoundItems));
+    for (int round = 0; round < rounds; ++round) {
+      const int r0 = round * kRoundItems;
+      if (round > 0) __syncthreads();  // the previous round is done with s_own
+      for (int k = t; k < n; k += kPlanThreads) {
+        const int lo = max(s_off[k], r0) - r0;
+        const int hi = min(s_off[k] + cdiv(s_sl[k], kPage) / chunk, r0 + kRoundItems) - r0;
+        for (int i = lo; i < hi; ++i) s_own[i] = k;
+      }
+      __syncthreads();
+
+      int item[kItemBatch + 1], first[kItemBatch + 1];
+      int4 rec[kItemBatch + 1];
+      const int k = round * kPlanThreads + t;
+      item[kItemBatch] = -1;
+      if (k < n) {
+        const int sq = base + k, g = s_sg[k], L = s_sl[k];
+        v.grp_members[atomicAdd(&s_cnt[g], 1)] = sq;
+        const int pages = cdiv(L, kPage), nfull = pages / chunk, rem = pages - nfull * chunk;
+        v.seq_parts[sq] = s_gpc[g] + nfull + (rem != 0 ? 1 : 0);
+        if (rem != 0) {
+          const int p0 = nfull * chunk;
+          item[kItemBatch] = atomicAdd(&s_hoff[rem], 1);
+          rec[kItemBatch] = make_int4(sq, p0, L - p0 * kPage, s_gpc[g] + nfull);
+          first[kItemBatch] = bt[(size_t)sq * a.max_resp_pages + p0];
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kItemBatch; ++u) {
+        const int i = r0 + u * kPlanThreads + t;
+        item[u] = -1;
+        if (i < (int)tot) {
+          const int o = s_own[i - r0];
+          const int sq = base + o, c = i - s_off[o], p0 = c * chunk;
+          item[u] = carry_f + i;
+          rec[u] = make_int4(sq, p0, min(chunk * kPage, s_sl[o] - p0 * kPage), s_gpc[s_sg[o]] + c);
+          first[u] = bt[(size_t)sq * a.max_resp_pages + p0];
+        }
+      }
+#pragma unroll
+      for (int u = 0; u <= kItemBatch; ++u) {
+        if (item[u] >= 0) {
+          v.resp_items[item[u]] = rec[u];
+          v.resp_first_page[item[u]] = first[u];
+        }
+      }
     }
-    v.hdr[kHdrRespItems] = off;
-    v.hdr[kHdrFullRespItems] = carry_f;
-  }
-  __syncthreads();
-  for (int s = t; s < S; s += kPlanThreads) {
-    const int L = clamp_len(a.resp_lens[s], a.max_resp_pages);
-    const int pages = cdiv(L, kPage);
-    const int rem = pages % chunk;
-    if (rem != 0) {
-      const int g = clamp_group(a.seq_to_group[s], G);
-      const int npc = prefix_chunks(a.prefix_lens[g], a.max_prefix_pages, v.max_prefix_chunks);
-      const int c = pages / chunk;
-      const int item = atomicAdd(&s_hoff[rem], 1);
-      v.resp_items[item] = make_int4(s, c, L, npc);
-      v.resp_first_page[item] = bt[(size_t)s * a.max_resp_pages + c * chunk];
-    }
+    carry_f += (int)tot;
   }
 }
 

@@ -150,3 +150,22 @@ def test_binding_raises_with_detail():
     with pytest.raises(rp.RpError) as e:
         B._check(rp.RP_ERR_UNSUPPORTED, "x")
     assert e.value.status == rp.RP_ERR_UNSUPPORTED
+
+
+def test_plan_layout_sections_fit_the_workspace():
+    kv, lay = _kv(), _layout(num_seqs=5, num_groups=2, mpp=3, mrp=70)
+    _, need = _ws_size(kv, lay)
+    info = B.plan_layout(kv, lay)
+    offs = [info.hdr, info.grp_off, info.grp_members, info.prefix_items, info.resp_items,
+            info.resp_first_page, info.seq_parts, info.part_o, info.part_lse]
+    assert offs == sorted(offs) and len(set(offs)) == len(offs)
+    assert all(o % 256 == 0 for o in offs)
+    # Capacities: 16-page prefix chunks, 32-page response pieces (the shorter B).
+    assert info.max_prefix_items == 2 * 1
+    assert info.max_resp_items == 5 * 3
+    assert info.parts_per_row == 1 + 3
+    assert info.max_parts == 5 * 4 * 4
+    assert info.part_lse + 4 * info.max_parts <= need
+    assert info.part_o + 4 * info.max_parts * 64 <= info.part_lse
+    with pytest.raises(B.RpError):
+        B.plan_layout(_kv(head_dim=96), lay)

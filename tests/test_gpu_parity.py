@@ -43,6 +43,12 @@ RAGGED = [
     ("no-prefix", 4, 2, 128, [0, 0], [0], [40, 1], "bf16"),
     ("fp8-edges", 16, 8, 128, [0, 0, 1, 1, 1], [33, 200], [0, 16, 17, 300, 513], "fp8"),
     ("fp8-d64-nrep4", 8, 2, 64, [0, 1, 0], [64, 9], [100, 31, 0], "fp8"),
+    # Response lengths on both sides of 32-page piece boundaries (short pieces).
+    ("piece-edges-short", 4, 2, 64, [0] * 5 + [1] * 4, [20, 0],
+     [497, 500, 511, 512, 513, 1008, 1009, 1023, 1024], "bf16"),
+    # Average above 256 pages, so 64-page pieces, with lengths at their edges.
+    ("piece-edges-long", 4, 2, 64, [0, 0, 0, 1, 1, 1, 1], [100, 16],
+     [4090, 4096, 4097, 8191, 8192, 1000, 12000], "bf16"),
 ]
 
 
@@ -69,6 +75,20 @@ def test_random_group_map_many_groups(kv_dtype):
     _, out, lse = run_hip(wl)
     ref_out, ref_lse, _ = run_oracle(wl)
     compare(out, lse, ref_out, ref_lse, kv_dtype, "random-map")
+
+
+def test_more_sequences_than_the_planner_caches():
+    # The planner keeps 8192 sequences' lengths in LDS and rereads the rest.
+    _say("8500 sequences")
+    rng = np.random.default_rng(91)
+    S, G = 8500, 300
+    s2g = rng.integers(0, G, size=S)
+    wl = make_workload(num_q_heads=2, num_kv_heads=1, head_dim=64, seq_to_group=s2g,
+                       prefix_lens=rng.integers(0, 40, size=G), resp_lens=rng.integers(0, 80, size=S),
+                       seed=6)
+    _, out, lse = run_hip(wl)
+    ref_out, ref_lse, _ = run_oracle(wl)
+    compare(out, lse, ref_out, ref_lse, "bf16", "8500-seqs")
 
 
 @pytest.mark.parametrize("kv_dtype", ["bf16", "fp8"])

@@ -1,0 +1,131 @@
+"""GPU: the work plan read back and checked against its contract, exactly.
+
+The planner's output is integer data, so every field is compared bit for bit
+with what the contract in include/rp.h fixes: prefix work items, member lists,
+the piece length B, every response cut into B-page pieces plus a shorter last
+piece, B-page pieces first in sequence order, then last pieces by decreasing
+page count, each item's slot and first physical page, and the part count per
+query row. Layouts are synthetic (lengths drawn like the benchmark workloads,
+block tables random over a small pool); the plan never reads K/V.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+pytestmark = pytest.mark.gpu
+
+PAGE, PREFIX_CHUNK, B_MIN, B_MAX, LONG_PAGES = 16, 16, 32, 64, 256
+
+
+def cdiv(a, b):
+    return -(-a // b)
+
+
+def make_batch(s2g, prefix_lens, resp_lens, num_groups, seed, num_pages=97, Hq=16, Hkv=8, d=128):
+    import paper_2606_26997_amd as rp
+    rng = np.random.default_rng(seed)
+    s2g = np.asarray(s2g, np.int32)
+    P = np.asarray(prefix_lens, np.int32)
+    L = np.asarray(resp_lens, np.int32)
+    mpp = max(1, cdiv(int(P.max(initial=0)), PAGE))
+    mrp = max(1, cdiv(int(L.max(initial=0)), PAGE))
+    pbt = rng.integers(0, num_pages, size=(num_groups, mpp), dtype=np.int32)
+    rbt = rng.integers(0, num_pages, size=(len(s2g), mrp), dtype=np.int32)
+    pool = torch.zeros((num_pages, Hkv, PAGE, d), dtype=torch.bfloat16)
+    q = torch.zeros((len(s2g), Hq, d), dtype=torch.bfloat16)
+    b = rp.DeviceBatch(k_pages=pool, v_pages=pool, k_scale=None, v_scale=None, seq_to_group=s2g,
+                       prefix_lens=P, prefix_block_table=pbt, resp_lens=L, resp_block_table=rbt, q=q,
+                       num_q_heads=Hq, softmax_scale=0.1)
+    return b, rbt
+
+
+def check_plan(b, s2g, P, L, rbt, G):
+    s2g, P, L = np.asarray(s2g), np.asarray(P, np.int64), np.asarray(L, np.int64)
+    S = len(s2g)
+    b.plan()
+    got = b.plan_contents()
+    hdr = got["hdr"]
+    pages = cdiv(L, PAGE)
+    B = B_MAX if pages.sum() >= S * LONG_PAGES else B_MIN
+    assert hdr[3] == B
+    live = np.bincount(s2g, minlength=G)
+    npc = cdiv(cdiv(P, PAGE), PREFIX_CHUNK)
+
+    want_prefix = [(g, c) for g in range(G) if live[g] > 0 for c in range(npc[g])]
+    assert hdr[0] == len(want_prefix)
+    assert [tuple(x) for x in got["prefix_items"]] == want_prefix
+
+    assert np.array_equal(got["grp_off"], np.concatenate([[0], np.cumsum(live)]))
+    for g in np.flatnonzero(live):
+        m = got["grp_members"][got["grp_off"][g]:got["grp_off"][g + 1]]
+        assert sorted(m.tolist()) == np.flatnonzero(s2g == g).tolist(), g
+
+    nfull = pages // B
+    ragged = pages % B != 0
+    assert hdr[2] == nfull.sum() and hdr[1] == nfull.sum() + ragged.sum()
+    items, first = got["resp_items"], got["resp_first_page"]
+    want_big = [(s, c * B, min(B * PAGE, L[s] - c * B * PAGE), npc[s2g[s]] + c)
+                for s in range(S) for c in range(nfull[s])]
+    assert [tuple(x) for x in items[:hdr[2]]] == want_big
+    tail = items[hdr[2]:]
+    want_tail = sorted((s, nfull[s] * B, L[s] - nfull[s] * B * PAGE, npc[s2g[s]] + nfull[s])
+                       for s in np.flatnonzero(ragged))
+    assert sorted(tuple(x) for x in tail) == want_tail
+    tail_pages = cdiv(tail[:, 2].astype(np.int64), PAGE)
+    assert np.all(np.diff(tail_pages) <= 0), "last pieces must come by decreasing page count"
+    assert np.all(tail_pages < B)
+    assert np.array_equal(first, rbt[items[:, 0], items[:, 1]])
+    assert np.array_equal(got["seq_parts"], npc[s2g] + cdiv(pages, B))
+
+
+def _case(name):
+    rng = np.random.default_rng(sum(map(ord, name)))
+    if name == "qwen-layer-uniform":        # 32 groups x 8, prefix U[64,512], resp U[0,4096]
+        G, S = 32, 256
+        s2g = np.repeat(np.arange(G), 8)
+        P, L = rng.integers(64, 513, G), rng.integers(0, 4097, S)
+    elif name == "lognormal-tail":          # 64 x 16, lognormal(1500, 0.9) capped at 8193
+        G, S = 64, 1024
+        s2g = np.repeat(np.arange(G), 16)
+        P = np.full(G, 256)
+        L = np.minimum(np.exp(rng.normal(np.log(1500), 0.9, S)).astype(np.int64), 8192) + 1
+    elif name == "frontier-random-map":     # 512 live of 128 groups, resp U[0,16384]
+        G, S = 128, 512
+        s2g = rng.integers(0, G, S)
+        P, L = rng.integers(128, 1025, G), rng.integers(0, 16385, S)
+    elif name == "long-context":            # 16 x 16, resp U[8192, 32768] + 1
+        G, S = 16, 256
+        s2g = np.repeat(np.arange(G), 16)
+        P, L = np.full(G, 256), rng.integers(8192, 32769, S) + 1
+    elif name == "many-sequences":          # several planner passes
+        G, S = 4096, 9000
+        s2g = rng.integers(0, G, S)
+        P, L = rng.integers(0, 300, G), rng.integers(0, 3000, S)
+    elif name == "many-pieces":             # several item rounds in one pass
+        G, S = 500, 4000
+        s2g = rng.integers(0, G, S)
+        P, L = rng.integers(0, 100, G), rng.integers(2000, 4000, S)
+    elif name == "empty-and-idle-groups":   # zero lengths, groups without members
+        G, S = 6, 5
+        s2g = np.array([0, 0, 3, 3, 5])
+        P, L = np.array([0, 17, 300, 0, 5, 16]), np.array([0, 512, 0, 513, 1])
+    else:
+        raise KeyError(name)
+    return G, s2g, P, L
+
+
+CASES = ["qwen-layer-uniform", "lognormal-tail", "frontier-random-map", "long-context", "many-sequences",
+         "many-pieces", "empty-and-idle-groups"]
+
+
+@pytest.mark.parametrize("name", CASES)
+def test_plan_matches_its_contract(name):
+    print(f"[case] plan {name}", flush=True)
+    sys.stdout.flush()
+    G, s2g, P, L = _case(name)
+    b, rbt = make_batch(s2g, P, L, G, seed=len(name))
+    check_plan(b, s2g, P, L, rbt, G)
+    # A second plan into the same workspace gives the same B-page items.
+    check_plan(b, s2g, P, L, rbt, G)
