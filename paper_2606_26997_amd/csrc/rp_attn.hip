@@ -30,6 +30,34 @@
 namespace rp {
 namespace {
 
+// Waves per work unit: the unit's pages are dealt round-robin to the waves of
+// one workgroup and the waves' softmax states are merged through LDS at the
+// end, so a unit drains kUnitWaves times faster without adding partial results.
+constexpr int kUnitWaves = 2;
+constexpr int kUnitThreads = 64 * kUnitWaves;
+
+// Orders this wave's LDS accesses (its staging area is its own).
+__device__ inline void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+}
+
+// LDS of one workgroup: the staged V page of each wave (prefix units), reused
+// for the waves' states while they merge, then the query tile of each wave
+// (prefix units). Row pitches are padded so that the column-wise and
+// row-wise reads of the MFMA operands do not collide on LDS banks.
+template <int D, int NREP>
+struct Smem {
+  static constexpr int kVStride = D + 4;  // staged V row pitch (bf16)
+  static constexpr int kQStride = D + 8;  // query tile row pitch (bf16)
+  static constexpr int kStage = kUnitWaves * kPage * kVStride * 2;
+  static constexpr int kPrefixMerge = (kUnitWaves - 1) * 64 * (2 + D / 16 * 4) * 4;
+  static constexpr int kRespMerge = (kUnitWaves - 1) * NREP * (D + 2) * 4;
+  static constexpr int kQOff = kStage > kPrefixMerge ? (kStage > kRespMerge ? kStage : kRespMerge)
+                                                     : (kPrefixMerge > kRespMerge ? kPrefixMerge : kRespMerge);
+  static constexpr int kBytes = kQOff + kUnitWaves * 16 * kQStride * 2;
+};
+
 // ---------------------------------------------------------------------------
 // Response path
 // ---------------------------------------------------------------------------
@@ -108,47 +136,82 @@ __device__ inline f32x4_t mfma16x16x16(const bf16x4_t& a, const bf16x4_t& b, con
                                                    c, 0, 0, 0);
 }
 
-// A operand of S^T = K Q^T for one page: lane (r16, quad) holds K[token r16][kb*32 + quad*8 + 0..7].
+// One page of a prefix unit in flight, as loaded (this lane's share):
+//  k: the A operand of S^T = K Q^T, lane (r16, quad) holds
+//     K[token r16][kb*32 + quad*8 + 0..7] (8 bf16, or 8 e4m3 codes);
+//  v: 16-byte pieces of the page's V block, lane-contiguous, for staging;
+//  ks, vs: the fp8 scales of the page.
 template <int D, bool FP8>
-__device__ inline void load_k_operand(const char* pool, size_t blk_bytes, int r16, int quad, bf16x8_t* op) {
+struct PrefixPage {
+  static constexpr int KB = D / 32;
+  static constexpr int VL = (FP8 ? kPage * D : kPage * D * 2) / 1024;
+  uint4 k[FP8 ? (KB + 1) / 2 : KB];
+  uint4 v[VL];
+  float ks, vs;
+};
+
+// Every load of the page is unconditional: padding rows of a ragged page are
+// read (they are inside the page) and masked when used.
+template <int D, bool FP8>
+__device__ inline void load_prefix_k(const AttnArgs& a, const char* kpool, int pg, int h, int lane,
+                                     PrefixPage<D, FP8>& r) {
+  constexpr size_t BLOCK_BYTES = (size_t)kPage * D * (FP8 ? 1 : 2);
+  const size_t blk = ((size_t)pg * a.num_kv_heads + h) * BLOCK_BYTES;
+  const int r16 = lane & 15, quad = lane >> 4;
 #pragma unroll
   for (int kb = 0; kb < D / 32; ++kb) {
     const int col = kb * 32 + quad * 8;
     if constexpr (!FP8) {
-      const uint4 w = *reinterpret_cast<const uint4*>(pool + blk_bytes + ((size_t)r16 * D + col) * 2);
-      op[kb] = __builtin_bit_cast(bf16x8_t, w);
+      r.k[kb] = *reinterpret_cast<const uint4*>(kpool + blk + ((size_t)r16 * D + col) * 2);
     } else {
-      const uint2 w = *reinterpret_cast<const uint2*>(pool + blk_bytes + (size_t)r16 * D + col);
-      op[kb] = __builtin_bit_cast(bf16x8_t, e4m3x8_to_bf16x8(w.x, w.y));
+      const uint2 w = *reinterpret_cast<const uint2*>(kpool + blk + (size_t)r16 * D + col);
+      if (kb % 2 == 0) { r.k[kb / 2].x = w.x; r.k[kb / 2].y = w.y; }
+      else { r.k[kb / 2].z = w.x; r.k[kb / 2].w = w.y; }
     }
+  }
+  if constexpr (FP8) r.ks = a.k_scale[(size_t)pg * a.num_kv_heads + h];
+}
+template <int D, bool FP8>
+__device__ inline void load_prefix_v(const AttnArgs& a, const char* vpool, int pg, int h, int lane,
+                                     PrefixPage<D, FP8>& r) {
+  constexpr size_t BLOCK_BYTES = (size_t)kPage * D * (FP8 ? 1 : 2);
+  const size_t blk = ((size_t)pg * a.num_kv_heads + h) * BLOCK_BYTES;
+#pragma unroll
+  for (int i = 0; i < PrefixPage<D, FP8>::VL; ++i)
+    r.v[i] = *reinterpret_cast<const uint4*>(vpool + blk + (size_t)i * 1024 + lane * 16);
+  if constexpr (FP8) r.vs = a.v_scale[(size_t)pg * a.num_kv_heads + h];
+}
+
+template <int D, bool FP8>
+__device__ inline bf16x8_t prefix_k_operand(const PrefixPage<D, FP8>& r, int kb) {
+  if constexpr (!FP8) {
+    return __builtin_bit_cast(bf16x8_t, r.k[kb]);
+  } else {
+    const uint4& w = r.k[kb / 2];
+    return __builtin_bit_cast(bf16x8_t, kb % 2 == 0 ? e4m3x8_to_bf16x8(w.x, w.y) : e4m3x8_to_bf16x8(w.z, w.w));
   }
 }
 
-// Copy one page's V block (bf16, or fp8 decoded to bf16) into LDS rows
+// Write the page's V block (bf16, or fp8 decoded to bf16) into LDS rows
 // 0..15; rows at or beyond `nvalid` are written as zeros.
 template <int D, bool FP8, int STRIDE>
-__device__ inline void stage_v(const char* pool, size_t blk_bytes, int nvalid, uint16_t* vt, int lane) {
-  if constexpr (!FP8) {
+__device__ inline void stage_v(const PrefixPage<D, FP8>& r, int nvalid, uint16_t* vt, int lane) {
 #pragma unroll
-    for (int i = 0; i < kPage * D * 2 / 1024; ++i) {
+  for (int i = 0; i < PrefixPage<D, FP8>::VL; ++i) {
+    if constexpr (!FP8) {
       const int e0 = i * 512 + lane * 8;
       const int tok = e0 / D, col = e0 % D;
-      uint4 w = make_uint4(0, 0, 0, 0);
-      if (tok < nvalid) w = *reinterpret_cast<const uint4*>(pool + blk_bytes + (size_t)e0 * 2);
+      const uint4 w = tok < nvalid ? r.v[i] : make_uint4(0, 0, 0, 0);
       uint2* dst = reinterpret_cast<uint2*>(vt + tok * STRIDE + col);
       dst[0] = make_uint2(w.x, w.y);
       dst[1] = make_uint2(w.z, w.w);
-    }
-  } else {
-#pragma unroll
-    for (int i = 0; i < kPage * D / 1024; ++i) {
+    } else {
       const int e0 = i * 1024 + lane * 16;
       const int tok = e0 / D, col = e0 % D;
       uint4 lo = make_uint4(0, 0, 0, 0), hi = make_uint4(0, 0, 0, 0);
       if (tok < nvalid) {
-        const uint4 w = *reinterpret_cast<const uint4*>(pool + blk_bytes + e0);
-        lo = e4m3x8_to_bf16x8(w.x, w.y);
-        hi = e4m3x8_to_bf16x8(w.z, w.w);
+        lo = e4m3x8_to_bf16x8(r.v[i].x, r.v[i].y);
+        hi = e4m3x8_to_bf16x8(r.v[i].z, r.v[i].w);
       }
       uint2* dst = reinterpret_cast<uint2*>(vt + tok * STRIDE + col);
       dst[0] = make_uint2(lo.x, lo.y);
@@ -164,14 +227,11 @@ __device__ inline void stage_v(const char* pool, size_t blk_bytes, int nvalid, u
 // step. A group with more than 16 query rows reads the chunk again for each
 // further pass; the chunk (a few tens of KiB) is then still in this XCD's L2.
 template <int D, int NREP, bool FP8>
-__device__ void prefix_unit(const AttnArgs& a, int item, int h, uint16_t* vt) {
+__device__ void prefix_unit(const AttnArgs& a, int item, int h, char* smem) {
   constexpr int KB = D / 32;       // MFMA k-blocks over head_dim
   constexpr int DT = D / 16;       // 16-column output tiles over head_dim
-  constexpr int STRIDE = D + 4;    // staged V row pitch (bf16 elements)
-  constexpr int EB = FP8 ? 1 : 2;
-  constexpr size_t BLOCK_BYTES = (size_t)kPage * D * EB;
-
-  const int Hkv = a.num_kv_heads;
+  constexpr int STRIDE = Smem<D, NREP>::kVStride;
+  constexpr int QSTRIDE = Smem<D, NREP>::kQStride;
   const int2 it = a.view.prefix_items[item];
   const int g = clamp_group(it.x, a.num_groups);
   const int c = min(max(it.y, 0), a.view.max_prefix_chunks - 1);
@@ -181,8 +241,11 @@ __device__ void prefix_unit(const AttnArgs& a, int item, int h, uint16_t* vt) {
   const int npages = cdiv(ntok, kPage);
   const int moff = a.view.grp_off[g];
   const int R = (a.view.grp_off[g + 1] - moff) * NREP;
-  const int lane = threadIdx.x;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r16 = lane & 15, quad = lane >> 4;
+  uint16_t* vt = reinterpret_cast<uint16_t*>(smem) + wave * (kPage * STRIDE);
+  uint16_t* qt = reinterpret_cast<uint16_t*>(smem + Smem<D, NREP>::kQOff) + wave * (16 * QSTRIDE);
+  uint16_t* qt_lane = qt + r16 * QSTRIDE + quad * 8;  // this lane's 16-byte pieces of its row
   const int* bt = a.prefix_block_table + (size_t)g * a.max_prefix_pages + c * kPrefixChunkPages;
   const char* kpool = static_cast<const char*>(a.k_pages);
   const char* vpool = static_cast<const char*>(a.v_pages);
@@ -196,40 +259,55 @@ __device__ void prefix_unit(const AttnArgs& a, int item, int h, uint16_t* vt) {
       const int sq = min(max(a.view.grp_members[moff + mem], 0), a.num_seqs - 1);
       rowid = sq * a.num_q_heads + h * NREP + rep;
     }
-    bf16x8_t qop[KB];
+    // The pass's query tile lives in this wave's LDS area (registers are the
+    // scarce resource); each page reads it back as the B operand of S^T.
+    wave_lds_sync();
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb) {
       uint4 w = make_uint4(0, 0, 0, 0);
       if (rowid >= 0) w = *reinterpret_cast<const uint4*>(qall + (size_t)rowid * D + kb * 32 + quad * 8);
-      qop[kb] = __builtin_bit_cast(bf16x8_t, w);
+      *reinterpret_cast<uint4*>(qt_lane + kb * 32) = w;
     }
+    wave_lds_sync();
 
     float mrow = -INFINITY, lrow = 0.f;
     f32x4_t oacc[DT];
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) oacc[dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-    for (int p = 0; p < npages; ++p) {
+    // Pages are software-pipelined: the next page's V is requested once this
+    // page's V is staged, its K once this page's scores exist (after this
+    // wave's last page, its last page again: cache hits).
+    PrefixPage<D, FP8> pg_regs;
+    if (wave < npages) {
+      const int pg0 = clamp_page(bt[wave], a.num_pages);
+      load_prefix_k<D, FP8>(a, kpool, pg0, h, lane, pg_regs);
+      load_prefix_v<D, FP8>(a, vpool, pg0, h, lane, pg_regs);
+    }
+    for (int p = wave; p < npages; p += kUnitWaves) {
       const int nv = min(kPage, ntok - p * kPage);
-      const int pg = clamp_page(bt[p], a.num_pages);
-      const size_t blk = ((size_t)pg * Hkv + h) * BLOCK_BYTES;
-
-      __syncthreads();  // the previous page's LDS reads are complete
-      stage_v<D, FP8, STRIDE>(vpool, blk, nv, vt, lane);
-
+      const int pn = clamp_page(bt[p + kUnitWaves < npages ? p + kUnitWaves : p], a.num_pages);
       float sm = a.qk_scale, vm = 1.f;
       if constexpr (FP8) {
-        sm *= a.k_scale[(size_t)pg * Hkv + h];
-        vm = a.v_scale[(size_t)pg * Hkv + h];
+        sm *= pg_regs.ks;
+        vm = pg_regs.vs;
       }
+
+      wave_lds_sync();  // the previous page's LDS reads are complete
+      stage_v<D, FP8, STRIDE>(pg_regs, nv, vt, lane);
+      // Keep each refill after the last use of the registers it overwrites.
+      __builtin_amdgcn_sched_barrier(0);
+      load_prefix_v<D, FP8>(a, vpool, pn, h, lane, pg_regs);
+
       // Entry i of this lane is token quad*4+i of the page and query row r16 of the tile.
       f32x4_t sacc = {0.f, 0.f, 0.f, 0.f};
-      {
-        bf16x8_t kop[KB];
-        load_k_operand<D, FP8>(kpool, blk, r16, quad, kop);
 #pragma unroll
-        for (int kb = 0; kb < KB; ++kb) sacc = mfma16x16x32(kop[kb], qop[kb], sacc);
+      for (int kb = 0; kb < KB; ++kb) {
+        const bf16x8_t qop = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(qt_lane + kb * 32));
+        sacc = mfma16x16x32(prefix_k_operand<D, FP8>(pg_regs, kb), qop, sacc);
       }
+      __builtin_amdgcn_sched_barrier(0);
+      load_prefix_k<D, FP8>(a, kpool, pn, h, lane, pg_regs);
       float x[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) x[i] = quad * 4 + i < nv ? sacc[i] * sm : -INFINITY;
@@ -250,7 +328,7 @@ __device__ void prefix_unit(const AttnArgs& a, int item, int h, uint16_t* vt) {
       const bf16x4_t pop = __builtin_bit_cast(
           bf16x4_t, make_uint2(pack_bf16x2(pw[0] * vm, pw[1] * vm), pack_bf16x2(pw[2] * vm, pw[3] * vm)));
 
-      __syncthreads();  // the staged V is visible to the whole wave
+      wave_lds_sync();  // the staged V is visible to the whole wave
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) {
         // A operand: V^T[column dt*16 + r16][k-slot quad*4 + j] = V[token quad*4 + j][column].
@@ -258,21 +336,62 @@ __device__ void prefix_unit(const AttnArgs& a, int item, int h, uint16_t* vt) {
         const uint32_t w0 = (uint32_t)col[0] | ((uint32_t)col[STRIDE] << 16);
         const uint32_t w1 = (uint32_t)col[2 * STRIDE] | ((uint32_t)col[3 * STRIDE] << 16);
         oacc[dt] = mfma16x16x16(__builtin_bit_cast(bf16x4_t, make_uint2(w0, w1)), pop, oacc[dt]);
+        // One tile's operand in flight at a time: the reads are cheap, registers are not.
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
 
-    const float lt = xor_sum_from<16>(lrow);
-    if (rowid >= 0) {
-      const int part = clamp_part(rowid * a.view.parts_per_row + c, a.view.max_parts);
-      const float inv = 1.f / lt;
-      float* dst = a.view.part_o + (size_t)part * D + quad * 4;
+    // Merge the waves' states lane by lane (every wave holds the same tile
+    // layout): waves 1.. publish theirs, wave 0 folds them in one output tile
+    // at a time and writes the partial.
+    constexpr int NF = 2 + DT * 4;
+    const float* xs = reinterpret_cast<const float*>(smem) + lane * NF;
+    if constexpr (kUnitWaves > 1) {
+      float* e = reinterpret_cast<float*>(smem) + ((wave - 1) * 64 + lane) * NF;
+      __syncthreads();  // every wave is done with its staged V
+      if (wave > 0) {
+        e[0] = mrow;
+        e[1] = lrow;
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-        const f32x4_t v = oacc[dt] * inv;
-        *reinterpret_cast<float4*>(dst + dt * 16) = make_float4(v[0], v[1], v[2], v[3]);
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) e[2 + dt * 4 + i] = oacc[dt][i];
       }
-      if (quad == 0) a.view.part_lse[part] = (mrow + fast_log2(lt)) * kLn2;
+      __syncthreads();
     }
+    if (wave == 0) {
+      float mx = mrow;
+#pragma unroll
+      for (int w = 1; w < kUnitWaves; ++w) mx = fmaxf(mx, xs[(w - 1) * 64 * NF]);
+      const float mu = mx == -INFINITY ? 0.f : mx;
+      const float a0 = fast_exp2(mrow - mu);
+      float aw[kUnitWaves];
+      float lsum = lrow * a0;
+#pragma unroll
+      for (int w = 1; w < kUnitWaves; ++w) {
+        aw[w] = fast_exp2(xs[(w - 1) * 64 * NF] - mu);
+        lsum += xs[(w - 1) * 64 * NF + 1] * aw[w];
+      }
+      const float lt = xor_sum_from<16>(lsum);
+      if (rowid >= 0) {
+        const int part = clamp_part(rowid * a.view.parts_per_row + c, a.view.max_parts);
+        const float inv = 1.f / lt;
+        float* dst = a.view.part_o + (size_t)part * D + quad * 4;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+          f32x4_t v = oacc[dt] * a0;
+#pragma unroll
+          for (int w = 1; w < kUnitWaves; ++w)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) v[i] += xs[(w - 1) * 64 * NF + 2 + dt * 4 + i] * aw[w];
+          v *= inv;
+          *reinterpret_cast<float4*>(dst + dt * 16) = make_float4(v[0], v[1], v[2], v[3]);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+        if (quad == 0) a.view.part_lse[part] = (mu + fast_log2(lt)) * kLn2;
+      }
+    }
+    if constexpr (kUnitWaves > 1) __syncthreads();  // the next pass may stage V over the merge area
   }
 }
 
@@ -281,11 +400,11 @@ __device__ void prefix_unit(const AttnArgs& a, int item, int h, uint16_t* vt) {
 // ---------------------------------------------------------------------------
 // One response unit: kv-head h of response item `item`.
 template <int D, int NREP, bool FP8>
-__device__ void resp_unit(const AttnArgs& a, int item, int h) {
+__device__ void resp_unit(const AttnArgs& a, int item, int h, char* smem) {
   using G = RespGeom<D, FP8>;
   constexpr int EPL = G::EPL, LPT = G::LPT, TPL = G::TPL, LOADS = G::LOADS, QW = G::QW;
   const int Hkv = a.num_kv_heads;
-  const int lane = threadIdx.x;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int tg = lane / LPT;
   const int sub = lane - tg * LPT;
   const char* kpool = static_cast<const char*>(a.k_pages);
@@ -299,7 +418,12 @@ __device__ void resp_unit(const AttnArgs& a, int item, int h) {
   const int ntok = min(max(m.z, 0), min(kRespChunkPagesMax, a.max_resp_pages - p0) * kPage);
   const int slot = min(max(m.w, 0), a.view.parts_per_row - 1);
   const int npages = cdiv(ntok, kPage);
+  const int* bt = a.resp_block_table + (size_t)s * a.max_resp_pages + p0;
+  // This wave takes pages wave, wave + kUnitWaves, ...; wave 0's first page id
+  // comes with the plan, the others' from the block table (a wave without
+  // pages loads the item's first page once and skips the loop).
   int page = clamp_page(a.view.resp_first_page[item], a.num_pages);
+  if (wave > 0 && wave < npages) page = clamp_page(bt[wave], a.num_pages);
   uint4 kr[LOADS], vr[LOADS];
   {
     const size_t blk = resp_block<D, FP8>(a, page, h, lane);
@@ -308,7 +432,6 @@ __device__ void resp_unit(const AttnArgs& a, int item, int h) {
 #pragma unroll
     for (int i = 0; i < LOADS; ++i) vr[i] = *reinterpret_cast<const uint4*>(vpool + blk + i * 1024);
   }
-  const int* bt = a.resp_block_table + (size_t)s * a.max_resp_pages + p0;
 
   // This lane's EPL head_dim elements of the NREP query rows of kv-head h (bf16).
   const uint16_t* qrow =
@@ -328,9 +451,9 @@ __device__ void resp_unit(const AttnArgs& a, int item, int h) {
     for (int e = 0; e < EPL; ++e) o[r][e] = 0.f;
   }
 
-  for (int p = 0; p < npages; ++p) {
-    // The following page (this one again after the last: a cache hit).
-    const int next_page = p + 1 < npages ? clamp_page(bt[p + 1], a.num_pages) : page;
+  for (int p = wave; p < npages; p += kUnitWaves) {
+    // This wave's following page (this one again after its last: a cache hit).
+    const int next_page = p + kUnitWaves < npages ? clamp_page(bt[p + kUnitWaves], a.num_pages) : page;
     const size_t next_blk = resp_block<D, FP8>(a, next_page, h, lane);
     const int nvalid = min(kPage, ntok - p * kPage);
     float smul = a.qk_scale, vmul = 1.f;
@@ -403,29 +526,59 @@ __device__ void resp_unit(const AttnArgs& a, int item, int h) {
     page = next_page;
   }
 
-  // Merge the TPL lane groups' states and write one partial per query row.
+  // Merge the TPL lane groups' states of each wave, then the waves' states
+  // (through LDS), and write one partial per query row.
   const int row0 = s * a.num_q_heads + h * NREP;
+  float* xs = reinterpret_cast<float*>(smem);  // [kUnitWaves - 1][NREP][D + 2]
 #pragma unroll
   for (int r = 0; r < NREP; ++r) {
-    const float M = xor_max_from<LPT>(mrun[r]);
+    float M = xor_max_from<LPT>(mrun[r]);
     const float Mu = M == -INFINITY ? 0.f : M;
     const float w = fast_exp2(mrun[r] - Mu);
-    const float lt = xor_sum_from<LPT>(l[r] * w);
-    const float inv = 1.f / lt;
+    float lt = xor_sum_from<LPT>(l[r] * w);
     float oo[EPL];
 #pragma unroll
-    for (int e = 0; e < EPL; ++e) oo[e] = xor_sum_from<LPT>(o[r][e] * w) * inv;
-    const int part = clamp_part((row0 + r) * a.view.parts_per_row + slot, a.view.max_parts);
-    if (tg == 0) {
-      float4* dst = reinterpret_cast<float4*>(a.view.part_o + (size_t)part * D + sub * EPL);
+    for (int e = 0; e < EPL; ++e) oo[e] = xor_sum_from<LPT>(o[r][e] * w);
+    if constexpr (kUnitWaves > 1) {
+      float* e0 = xs + ((size_t)r * (kUnitWaves - 1) + (wave - 1)) * (D + 2);
+      if (wave > 0 && tg == 0) {
 #pragma unroll
-      for (int e = 0; e < EPL; e += 4) dst[e / 4] = make_float4(oo[e], oo[e + 1], oo[e + 2], oo[e + 3]);
+        for (int e = 0; e < EPL; ++e) e0[2 + sub * EPL + e] = oo[e];
+        if (sub == 0) {
+          e0[0] = M;
+          e0[1] = lt;
+        }
+      }
+      __syncthreads();
+      if (wave == 0 && tg == 0) {
+#pragma unroll
+        for (int w2 = 1; w2 < kUnitWaves; ++w2) {
+          const float* e1 = xs + ((size_t)r * (kUnitWaves - 1) + (w2 - 1)) * (D + 2);
+          const float m1 = e1[0];
+          const float mx = fmaxf(M, m1);
+          const float mu = mx == -INFINITY ? 0.f : mx;
+          const float a0 = fast_exp2(M - mu), a1 = fast_exp2(m1 - mu);
+          lt = lt * a0 + e1[1] * a1;
+#pragma unroll
+          for (int e = 0; e < EPL; ++e) oo[e] = oo[e] * a0 + e1[2 + sub * EPL + e] * a1;
+          M = mx;
+        }
+      }
     }
-    if (lane == 0) a.view.part_lse[part] = (M + fast_log2(lt)) * kLn2;
+    if (wave == 0) {
+      const int part = clamp_part((row0 + r) * a.view.parts_per_row + slot, a.view.max_parts);
+      const float inv = 1.f / lt;
+      if (tg == 0) {
+        float4* dst = reinterpret_cast<float4*>(a.view.part_o + (size_t)part * D + sub * EPL);
+#pragma unroll
+        for (int e = 0; e < EPL; e += 4) dst[e / 4] = make_float4(oo[e] * inv, oo[e + 1] * inv, oo[e + 2] * inv, oo[e + 3] * inv);
+      }
+      if (lane == 0) a.view.part_lse[part] = (M + fast_log2(lt)) * kLn2;
+    }
   }
 }
 
-// All partial results in one launch, one unit per one-wave block: the first
+// All partial results in one launch, one unit per workgroup: the first
 // blocks take the group-prefix units (dispatched first; their short,
 // latency-bound MFMA work overlaps the response units that fill the rest of
 // the GPU), the following blocks the response units in plan order (big items
@@ -436,21 +589,21 @@ __device__ void resp_unit(const AttnArgs& a, int item, int h) {
 // counts are clamped to the plan's capacity, so even a workspace that was
 // never planned cannot send a wave outside the item lists.
 template <int D, int NREP, bool FP8>
-__global__ __launch_bounds__(64) void attn_parts_kernel(const AttnArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t vt[kPage * (D + 4)];
+__global__ __launch_bounds__(kUnitThreads) void attn_parts_kernel(const AttnArgs a) {
+  __shared__ __attribute__((aligned(16))) char smem[Smem<D, NREP>::kBytes];
   const int Hkv = a.num_kv_heads;
   const int n_pre = min(max(a.view.hdr[kHdrPrefixItems], 0), a.view.max_prefix_items) * Hkv;
   const int n_resp = min(max(a.view.hdr[kHdrRespItems], 0), a.view.max_resp_items) * Hkv;
   const int b = blockIdx.x;
   if (b < n_pre) {
     const int item = b / Hkv;
-    prefix_unit<D, NREP, FP8>(a, item, b - item * Hkv, vt);
+    prefix_unit<D, NREP, FP8>(a, item, b - item * Hkv, smem);
     return;
   }
   const int resp = b - n_pre;
   if (resp < n_resp) {
     const int item = resp / Hkv;
-    resp_unit<D, NREP, FP8>(a, item, resp - item * Hkv);
+    resp_unit<D, NREP, FP8>(a, item, resp - item * Hkv, smem);
   }
 }
 
@@ -458,7 +611,7 @@ __global__ __launch_bounds__(64) void attn_parts_kernel(const AttnArgs a) {
 template <int D, int NREP, bool FP8>
 hipError_t launch_one(const AttnArgs& a, long long prefix_blocks, long long resp_blocks, hipStream_t st) {
   const long long blocks = prefix_blocks + resp_blocks;
-  attn_parts_kernel<D, NREP, FP8><<<dim3((unsigned)blocks), dim3(64), 0, st>>>(a);
+  attn_parts_kernel<D, NREP, FP8><<<dim3((unsigned)blocks), dim3(kUnitThreads), 0, st>>>(a);
   return hipGetLastError();
 }
 
