@@ -42,7 +42,7 @@ def parse_args():
     p.add_argument("--warmup", type=int, default=10)
     p.add_argument("--config", type=int, default=2, help="workload number 1-5 (default 2)")
     p.add_argument("--seed", type=int, default=None)
-    p.add_argument("--cpu-seconds", type=float, default=15.0,
+    p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="wall-clock budget of the oracle CPU baseline sample (0 disables it)")
     p.add_argument("--copy-calibration", action="store_true",
                    help="run only a plain device copy of known size (for HBM counter scaling)")
@@ -90,13 +90,14 @@ def byte_model(wl):
     return out
 
 
-def load_traffic():
-    """HBM traffic of the partial-attention kernel from stored rocprofv3 counter runs, if current."""
+def load_traffic(workload):
+    """HBM traffic of the partial-attention kernel from stored rocprofv3 counter runs, if they
+    were taken on this workload with the current kernel sources."""
     if not os.path.exists(TRAFFIC_FILE):
         return None
     with open(TRAFFIC_FILE) as f:
         t = json.load(f)
-    if t.get("source_hash") != kernel_source_hash():
+    if t.get("source_hash") != kernel_source_hash() or t.get("workload") != workload:
         return None
     return t.get("traffic_bytes_per_launch")
 
@@ -116,22 +117,22 @@ def cpu_baseline(wl, budget_s, bytes_per_step):
         t0 = time.perf_counter()
         pool = append_for_workload(wl)
         t_app = time.perf_counter() - t0
+    # Sequences in a random order, in repeated passes, until the budget is spent.
     order = np.random.default_rng(0).permutation(wl.num_seqs)
     done = 0
     with threadpool_limits(limits=1):
         t0 = time.perf_counter()
-        for s in order:
-            oracle.attention_for_workload(wl, seqs=[int(s)], pool=pool)
+        while time.perf_counter() - t0 < budget_s:
+            oracle.attention_for_workload(wl, seqs=[int(order[done % wl.num_seqs])], pool=pool)
             done += 1
-            if time.perf_counter() - t0 >= budget_s:
-                break
         el = time.perf_counter() - t0
     seq_steps_per_s = done / (el + t_app * done / wl.num_seqs)
     return {"value": round(bytes_per_step / wl.num_seqs * seq_steps_per_s / 1e9, 4), "unit": "GB/s",
             "cores": 1, "kind": "oracle",
-            "sample": f"fp64 numpy oracle on {done} of {wl.num_seqs} sequences (random order, "
-                      f"{el:.1f} s, 1 thread{', append on the whole pool' if wl.append else ''}); "
-                      f"scaled by the step's algorithmic bytes per sequence",
+            "sample": f"fp64 numpy oracle, {done} sequence-steps ({done / wl.num_seqs:.1f} passes over the "
+                      f"{wl.num_seqs} sequences of the workload in random order, {el:.1f} s, 1 thread"
+                      f"{', plus the append on the whole pool' if wl.append else ''}); scaled by the "
+                      f"step's algorithmic bytes per sequence",
             "seq_steps_per_s": round(seq_steps_per_s, 3)}
 
 
@@ -257,7 +258,7 @@ def main():
 
     gbps = bm["total"] / (ms_per_step * 1e-3) / 1e9
     achieved = bm["parts_kernel"] / (parts_us * 1e-6) / 1e9
-    traffic = load_traffic()
+    traffic = load_traffic(f"config{cfg.cid}") if args.seed is None else None
     cpu = None
     if args.cpu_seconds > 0:
         print("[bench] timing the oracle CPU baseline", file=sys.stderr, flush=True)
