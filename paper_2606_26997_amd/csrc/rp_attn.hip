@@ -36,6 +36,16 @@ namespace {
 constexpr int kUnitWaves = 2;
 constexpr int kUnitThreads = 64 * kUnitWaves;
 
+// V pages are read with the non-temporal hint and K pages without it: both
+// streams are read exactly once, and marking one of the two (either one) as
+// streaming was measured 6-8% faster on every workload than marking neither
+// or both.
+typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+__device__ inline uint4 load_v_stream(const char* p) {
+  const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
+  return make_uint4(v[0], v[1], v[2], v[3]);
+}
+
 // Orders this wave's LDS accesses (its staging area is its own).
 __device__ inline void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
@@ -178,7 +188,7 @@ __device__ inline void load_prefix_v(const AttnArgs& a, const char* vpool, int p
   const size_t blk = ((size_t)pg * a.num_kv_heads + h) * BLOCK_BYTES;
 #pragma unroll
   for (int i = 0; i < PrefixPage<D, FP8>::VL; ++i)
-    r.v[i] = *reinterpret_cast<const uint4*>(vpool + blk + (size_t)i * 1024 + lane * 16);
+    r.v[i] = load_v_stream(vpool + blk + (size_t)i * 1024 + lane * 16);
   if constexpr (FP8) r.vs = a.v_scale[(size_t)pg * a.num_kv_heads + h];
 }
 
@@ -430,7 +440,7 @@ __device__ void resp_unit(const AttnArgs& a, int item, int h, char* smem) {
 #pragma unroll
     for (int i = 0; i < LOADS; ++i) kr[i] = *reinterpret_cast<const uint4*>(kpool + blk + i * 1024);
 #pragma unroll
-    for (int i = 0; i < LOADS; ++i) vr[i] = *reinterpret_cast<const uint4*>(vpool + blk + i * 1024);
+    for (int i = 0; i < LOADS; ++i) vr[i] = load_v_stream(vpool + blk + i * 1024);
   }
 
   // This lane's EPL head_dim elements of the NREP query rows of kv-head h (bf16).
@@ -486,7 +496,7 @@ __device__ void resp_unit(const AttnArgs& a, int item, int h, char* smem) {
       else unpack_e4m3x16(vr[i], vf[i]);
     }
 #pragma unroll
-    for (int i = 0; i < LOADS; ++i) vr[i] = *reinterpret_cast<const uint4*>(vpool + next_blk + i * 1024);
+    for (int i = 0; i < LOADS; ++i) vr[i] = load_v_stream(vpool + next_blk + i * 1024);
 
     if (nvalid < kPage) {  // ragged last page: padding rows may hold anything
 #pragma unroll
