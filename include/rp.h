@@ -191,12 +191,11 @@ rp_status rp_combine_parts(const rp_paged_kv* kv, const rp_group_layout* layout,
  *   prefix_items: (group, chunk of 16 prefix pages) pairs;
  *   resp_items: (sequence, first page index in the sequence's block table,
  *               tokens, partial-result slot) quadruples, in dispatch order;
- *   resp_first_page: the physical page id of each response item's first page;
  *   seq_parts[S]: partial results per query row of each sequence.
  * part_o (fp32 [max_parts][head_dim]) and part_lse (fp32 [max_parts]) hold
  * the partial results of query row r in slots r * parts_per_row + k. */
 typedef struct {
-  size_t hdr, grp_off, grp_members, prefix_items, resp_items, resp_first_page, seq_parts;
+  size_t hdr, grp_off, grp_members, prefix_items, resp_items, seq_parts;
   size_t part_o, part_lse;
   int32_t max_prefix_items, max_resp_items, parts_per_row, max_parts;
 } rp_plan_info;

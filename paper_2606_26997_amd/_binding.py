@@ -49,7 +49,7 @@ class RpGroupLayout(ctypes.Structure):
 
 class RpPlanInfo(ctypes.Structure):
     _fields_ = [(n, ctypes.c_size_t) for n in ("hdr", "grp_off", "grp_members", "prefix_items", "resp_items",
-                                                 "resp_first_page", "seq_parts", "part_o", "part_lse")] + \
+                                                 "seq_parts", "part_o", "part_lse")] + \
                [(n, ctypes.c_int32) for n in ("max_prefix_items", "max_resp_items", "parts_per_row", "max_parts")]
 
 

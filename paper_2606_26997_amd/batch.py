@@ -119,7 +119,6 @@ class DeviceBatch:
         return dict(hdr=hdr, grp_off=arr(info.grp_off, G + 1), grp_members=arr(info.grp_members, S),
                     prefix_items=arr(info.prefix_items, int(hdr[0]), 2),
                     resp_items=arr(info.resp_items, int(hdr[1]), 4),
-                    resp_first_page=arr(info.resp_first_page, int(hdr[1])),
                     seq_parts=arr(info.seq_parts, S), parts_per_row=info.parts_per_row)
 
     def validate(self, stream=None):

@@ -100,7 +100,7 @@ rp_status check_shape(const rp_paged_kv* kv, const rp_group_layout* l, Shape* sh
 
 // Workspace layout, 256-byte aligned sections.
 struct WsLayout {
-  size_t hdr, grp_off, members, pitems, ritems, rpage0, seq_parts, part_o, part_lse, total;
+  size_t hdr, grp_off, members, pitems, ritems, seq_parts, part_o, part_lse, total;
   long long max_pitems, max_ritems, max_parts;
   int max_pc, max_rc;
 };
@@ -123,7 +123,6 @@ bool ws_layout(const Shape& sh, WsLayout* w) {
   w->members = o;   o = align_up(o + sizeof(int) * (size_t)sh.S);
   w->pitems = o;    o = align_up(o + sizeof(int2) * (size_t)w->max_pitems);
   w->ritems = o;    o = align_up(o + sizeof(int4) * (size_t)w->max_ritems);
-  w->rpage0 = o;    o = align_up(o + sizeof(int) * (size_t)w->max_ritems);
   w->seq_parts = o; o = align_up(o + sizeof(int) * (size_t)sh.S);
   w->part_o = o;    o = align_up(o + sizeof(float) * (size_t)w->max_parts * sh.D);
   w->part_lse = o;  o = align_up(o + sizeof(float) * (size_t)w->max_parts);
@@ -139,7 +138,6 @@ rp::PlanView plan_view(void* ws, const WsLayout& w) {
   v.grp_members = reinterpret_cast<int*>(b + w.members);
   v.prefix_items = reinterpret_cast<int2*>(b + w.pitems);
   v.resp_items = reinterpret_cast<int4*>(b + w.ritems);
-  v.resp_first_page = reinterpret_cast<int*>(b + w.rpage0);
   v.seq_parts = reinterpret_cast<int*>(b + w.seq_parts);
   v.part_o = reinterpret_cast<float*>(b + w.part_o);
   v.part_lse = reinterpret_cast<float*>(b + w.part_lse);
@@ -235,8 +233,6 @@ rp_status rp_plan(const rp_paged_kv* kv, const rp_group_layout* l, void* ws, siz
   a.seq_to_group = l->seq_to_group;
   a.prefix_lens = l->prefix_lens;
   a.resp_lens = l->resp_lens;
-  a.resp_block_table = l->resp_block_table;
-  a.num_pages = sh.num_pages;
   a.max_prefix_pages = sh.max_pp;
   a.max_resp_pages = sh.max_rp;
   a.view = plan_view(ws, w);
@@ -362,7 +358,6 @@ rp_status rp_plan_layout(const rp_paged_kv* kv, const rp_group_layout* l, rp_pla
   info->grp_members = w.members;
   info->prefix_items = w.pitems;
   info->resp_items = w.ritems;
-  info->resp_first_page = w.rpage0;
   info->seq_parts = w.seq_parts;
   info->part_o = w.part_o;
   info->part_lse = w.part_lse;

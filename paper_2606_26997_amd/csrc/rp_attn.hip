@@ -420,8 +420,7 @@ __device__ void resp_unit(const AttnArgs& a, int item, int h, char* smem) {
   const char* kpool = static_cast<const char*>(a.k_pages);
   const char* vpool = static_cast<const char*>(a.v_pages);
 
-  // The item record (sequence, first page, tokens, slot) and its first page id
-  // come straight from the plan, so the first K/V loads depend on one load only.
+  // The item record: sequence, first page index in its block table, tokens, slot.
   const int4 m = a.view.resp_items[item];
   const int s = min(max(m.x, 0), a.num_seqs - 1);
   const int p0 = min(max(m.y, 0), a.max_resp_pages);
@@ -429,11 +428,9 @@ __device__ void resp_unit(const AttnArgs& a, int item, int h, char* smem) {
   const int slot = min(max(m.w, 0), a.view.parts_per_row - 1);
   const int npages = cdiv(ntok, kPage);
   const int* bt = a.resp_block_table + (size_t)s * a.max_resp_pages + p0;
-  // This wave takes pages wave, wave + kUnitWaves, ...; wave 0's first page id
-  // comes with the plan, the others' from the block table (a wave without
-  // pages loads the item's first page once and skips the loop).
-  int page = clamp_page(a.view.resp_first_page[item], a.num_pages);
-  if (wave > 0 && wave < npages) page = clamp_page(bt[wave], a.num_pages);
+  // This wave takes pages wave, wave + kUnitWaves, ...; a wave without pages
+  // loads the item's first page once and skips the loop.
+  int page = npages > 0 ? clamp_page(bt[wave < npages ? wave : 0], a.num_pages) : 0;
   uint4 kr[LOADS], vr[LOADS];
   {
     const size_t blk = resp_block<D, FP8>(a, page, h, lane);

@@ -54,7 +54,6 @@ struct PlanView {
   int* grp_members;    // [S]   members of each group in ascending order of arrival
   int2* prefix_items;  // [max_prefix_items]  (group, chunk)
   int4* resp_items;    // [max_resp_items]    (sequence, first page, tokens, slot), longest first
-  int* resp_first_page;  // [max_resp_items]  physical page of each response item's first page
   int* seq_parts;      // [S] partial results per query row of each sequence
   float* part_o;       // [S*Hq*parts_per_row][D]
   float* part_lse;     // [S*Hq*parts_per_row]

@@ -24,11 +24,10 @@ __device__ inline int clamp_page(int p, int num_pages) {
 }
 
 struct PlanArgs {
-  int num_seqs, num_groups, num_q_heads, num_pages;
+  int num_seqs, num_groups, num_q_heads;
   const int* seq_to_group;
   const int* prefix_lens;
   const int* resp_lens;
-  const int* resp_block_table;
   int max_prefix_pages, max_resp_pages;
   PlanView view;
 };

@@ -4,9 +4,8 @@
 //    groups with at least one live member,
 //  * the piece length B for this batch (from the average response length),
 //  * the number of partial results per query row of each sequence,
-//  * response work items (sequence, first page, tokens, partial-result slot)
-//    with the physical id of each item's first page: every B-page piece
-//    first, then the ragged last pieces by decreasing size.
+//  * response work items (sequence, first page, tokens, partial-result slot):
+//    every B-page piece first, then the ragged last pieces by decreasing size.
 // Group counters live in LDS; scans are wavefront scans plus one pass over
 // the wave totals.
 #include "rp_device.h"
@@ -61,8 +60,7 @@ __device__ inline int lo32(long long v) { return (int)(v & 0xFFFFFFFFll); }
 // in LDS (a batch with more sequences takes several passes).
 constexpr int kPlanSeqBlock = 4096;
 constexpr int kSeqPerThread = kPlanSeqBlock / kPlanThreads;
-// B-sized pieces written per thread per round; their block-table loads are
-// issued together with those of the thread's ragged pieces.
+// B-sized pieces written per thread per round.
 constexpr int kItemBatch = 8;
 constexpr int kRoundItems = kItemBatch * kPlanThreads;
 
@@ -81,7 +79,6 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
   const int t = threadIdx.x, lane = t & 63;
   const int S = a.num_seqs, G = a.num_groups;
   const PlanView v = a.view;
-  const int* bt = a.resp_block_table;
 
   for (int g = t; g < G; g += kPlanThreads) s_cnt[g] = 0;
   if (t < 2 * kRespChunkPagesMax) s_hist[t / kRespChunkPagesMax][t % kRespChunkPagesMax] = 0;
@@ -199,7 +196,9 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
     // Rounds of kRoundItems B-sized pieces: the owner of every piece of the
     // round goes into LDS first, then thread t writes pieces t + u *
     // kPlanThreads of the round, plus the member slot and ragged piece of
-    // sequences t + round * kPlanThreads, all block-table loads in one batch.
+    // sequences t + round * kPlanThreads. Items hold no physical page ids:
+    // gathering them from the block tables here would make one CU fetch a
+    // cache line per item.
     const int rounds = max(cdiv(n, kPlanThreads), cdiv((int)tot, kRoundItems));
     for (int round = 0; round < rounds; ++round) {
       const int r0 = round * kRoundItems;
@@ -211,7 +210,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
       }
       __syncthreads();
 
-      int item[kItemBatch + 1], first[kItemBatch + 1];
+      int item[kItemBatch + 1];
       int4 rec[kItemBatch + 1];
       const int k = round * kPlanThreads + t;
       item[kItemBatch] = -1;
@@ -224,7 +223,6 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
           const int p0 = nfull * chunk;
           item[kItemBatch] = atomicAdd(&s_hoff[rem], 1);
           rec[kItemBatch] = make_int4(sq, p0, L - p0 * kPage, s_gpc[g] + nfull);
-          first[kItemBatch] = bt[(size_t)sq * a.max_resp_pages + p0];
         }
       }
 #pragma unroll
@@ -236,15 +234,11 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
           const int sq = base + o, c = i - s_off[o], p0 = c * chunk;
           item[u] = carry_f + i;
           rec[u] = make_int4(sq, p0, min(chunk * kPage, s_sl[o] - p0 * kPage), s_gpc[s_sg[o]] + c);
-          first[u] = bt[(size_t)sq * a.max_resp_pages + p0];
         }
       }
 #pragma unroll
       for (int u = 0; u <= kItemBatch; ++u) {
-        if (item[u] >= 0) {
-          v.resp_items[item[u]] = rec[u];
-          v.resp_first_page[item[u]] = first[u];
-        }
+        if (item[u] >= 0) v.resp_items[item[u]] = rec[u];
       }
     }
     carry_f += (int)tot;

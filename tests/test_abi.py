@@ -157,7 +157,7 @@ def test_plan_layout_sections_fit_the_workspace():
     _, need = _ws_size(kv, lay)
     info = B.plan_layout(kv, lay)
     offs = [info.hdr, info.grp_off, info.grp_members, info.prefix_items, info.resp_items,
-            info.resp_first_page, info.seq_parts, info.part_o, info.part_lse]
+            info.seq_parts, info.part_o, info.part_lse]
     assert offs == sorted(offs) and len(set(offs)) == len(offs)
     assert all(o % 256 == 0 for o in offs)
     # Capacities: 16-page prefix chunks, 32-page response pieces (the shorter B).

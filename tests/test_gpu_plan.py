@@ -4,8 +4,7 @@ The planner's output is integer data, so every field is compared bit for bit
 with what the contract in include/rp.h fixes: prefix work items, member lists,
 the piece length B, every response cut into B-page pieces plus a shorter last
 piece, B-page pieces first in sequence order, then last pieces by decreasing
-page count, each item's slot and first physical page, and the part count per
-query row. Layouts are synthetic (lengths drawn like the benchmark workloads,
+page count, each item's slot, and the part count per query row. Layouts are synthetic (lengths drawn like the benchmark workloads,
 block tables random over a small pool); the plan never reads K/V.
 """
 import sys
@@ -65,7 +64,7 @@ def check_plan(b, s2g, P, L, rbt, G):
     nfull = pages // B
     ragged = pages % B != 0
     assert hdr[2] == nfull.sum() and hdr[1] == nfull.sum() + ragged.sum()
-    items, first = got["resp_items"], got["resp_first_page"]
+    items = got["resp_items"]
     want_big = [(s, c * B, min(B * PAGE, L[s] - c * B * PAGE), npc[s2g[s]] + c)
                 for s in range(S) for c in range(nfull[s])]
     assert [tuple(x) for x in items[:hdr[2]]] == want_big
@@ -76,7 +75,6 @@ def check_plan(b, s2g, P, L, rbt, G):
     tail_pages = cdiv(tail[:, 2].astype(np.int64), PAGE)
     assert np.all(np.diff(tail_pages) <= 0), "last pieces must come by decreasing page count"
     assert np.all(tail_pages < B)
-    assert np.array_equal(first, rbt[items[:, 0], items[:, 1]])
     assert np.array_equal(got["seq_parts"], npc[s2g] + cdiv(pages, B))
 
 
