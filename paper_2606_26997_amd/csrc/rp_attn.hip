@@ -32,8 +32,10 @@ namespace {
 
 // Waves per work unit: the unit's pages are dealt round-robin to the waves of
 // one workgroup and the waves' softmax states are merged through LDS at the
-// end, so a unit drains kUnitWaves times faster without adding partial results.
-constexpr int kUnitWaves = 2;
+// end, so a unit drains kUnitWaves times faster without adding partial
+// results. One wave per unit measured best once V is read non-temporally (two
+// waves tie on short responses and lose 1-2% on long ones).
+constexpr int kUnitWaves = 1;
 constexpr int kUnitThreads = 64 * kUnitWaves;
 
 // V pages are read with the non-temporal hint and K pages without it: both
