@@ -75,6 +75,7 @@ def check_plan(b, s2g, P, L, rbt, G):
     tail_pages = cdiv(tail[:, 2].astype(np.int64), PAGE)
     assert np.all(np.diff(tail_pages) <= 0), "last pieces must come by decreasing page count"
     assert np.all(tail_pages < B)
+    return B
     assert np.array_equal(got["seq_parts"], npc[s2g] + cdiv(pages, B))
 
 
@@ -105,6 +106,14 @@ def _case(name):
         G, S = 500, 4000
         s2g = rng.integers(0, G, S)
         P, L = rng.integers(0, 100, G), rng.integers(2000, 4000, S)
+    elif name == "frontier-dispatch-16":    # 2 groups x 8 live sequences (the paper's F_w = 2, K = 8)
+        G, S = 2, 16
+        s2g = np.repeat(np.arange(G), 8)
+        P, L = rng.integers(64, 513, G), rng.integers(3000, 4001, S)
+    elif name == "few-long-sequences":      # average >= 256 pages over only 8 sequences
+        G, S = 2, 8
+        s2g = np.repeat(np.arange(G), 4)
+        P, L = np.array([100, 300]), rng.integers(6000, 9000, S)
     elif name == "empty-and-idle-groups":   # zero lengths, groups without members
         G, S = 6, 5
         s2g = np.array([0, 0, 3, 3, 5])
@@ -115,7 +124,7 @@ def _case(name):
 
 
 CASES = ["qwen-layer-uniform", "lognormal-tail", "frontier-random-map", "long-context", "many-sequences",
-         "many-pieces", "empty-and-idle-groups"]
+         "many-pieces", "frontier-dispatch-16", "few-long-sequences", "empty-and-idle-groups"]
 
 
 @pytest.mark.parametrize("name", CASES)
@@ -124,6 +133,10 @@ def test_plan_matches_its_contract(name):
     sys.stdout.flush()
     G, s2g, P, L = _case(name)
     b, rbt = make_batch(s2g, P, L, G, seed=len(name))
-    check_plan(b, s2g, P, L, rbt, G)
+    B = check_plan(b, s2g, P, L, rbt, G)
+    if name in ("qwen-layer-uniform", "lognormal-tail", "frontier-dispatch-16"):
+        assert B == 32, B
+    if name in ("frontier-random-map", "long-context", "few-long-sequences"):
+        assert B == 64, B
     # A second plan into the same workspace gives the same B-page items.
     check_plan(b, s2g, P, L, rbt, G)
