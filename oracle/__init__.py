@@ -12,6 +12,8 @@ Everything is computed in float64 from the plain definitions:
 * the log-sum-exp merge of partial results over disjoint key subsets;
 * the KV append (bf16 copy, or OCP e4m3fn quantisation with a per-(page, head)
   scale);
+* the shared-prefix prefill: causal attention over each group's prompt and
+  the one-time write of its K/V pages;
 * bf16 and OCP e4m3fn decoding from the formats' bit definitions.
 
 Every function here is pinned by ``-m "not gpu"`` tests against library
@@ -21,7 +23,8 @@ from .formats import bf16_to_f64, bf16_to_f32, e4m3_to_f64, e4m3_encode, E4M3_MA
 from .attention import decode_attention, key_slots, attention_for_workload
 from .combine import lse_combine
 from .append import kv_append, append_for_workload
+from .prefill import prefill_attention, prefill_kv_write
 
 __all__ = ["bf16_to_f64", "bf16_to_f32", "e4m3_to_f64", "e4m3_encode", "E4M3_MAX",
            "decode_attention", "key_slots", "attention_for_workload",
-           "lse_combine", "kv_append", "append_for_workload"]
+           "lse_combine", "kv_append", "append_for_workload", "prefill_attention", "prefill_kv_write"]
