@@ -151,6 +151,46 @@ rp_status rp_lse_combine(const float* o_parts, const float* lse_parts,
                          const int32_t* row_part_offsets, int32_t num_rows, int32_t head_dim,
                          void* out, float* lse_out, hipStream_t stream);
 
+/* ---- Shared-prefix prefill ---------------------------------------------
+ * Every response of a GRPO group is sampled from the same prompt (paper,
+ * Section 2.1), so a prompt is processed once per group, not once per
+ * response: its K/V are written once into the group's prefix pages (the pages
+ * rp_group_decode_attn reads for every response of the group) and its tokens
+ * attend causally within the prompt.
+ *
+ * Prompt tokens of all groups are packed: group g owns rows
+ * prompt_offs[g] .. prompt_offs[g+1]-1 of q [T][Hq][head_dim] and
+ * k, v [T][Hkv][head_dim] (bf16), its prompt length being the difference;
+ * token t of group g lives at page prefix_block_table[g][t / 16], row t % 16. */
+typedef struct {
+  int32_t num_groups;                 /* G */
+  int32_t num_q_heads;                /* Hq; Hkv and head_dim come from the pool */
+  int32_t num_tokens;                 /* T = prompt_offs[G], a host copy */
+  const int32_t* prompt_offs;         /* [G + 1], non-decreasing, prompt_offs[0] = 0 */
+  const int32_t* prefix_block_table;  /* [G][max_prefix_pages] */
+  int32_t max_prefix_pages;           /* every prompt has at most max_prefix_pages * 16 tokens */
+} rp_prefill_layout;
+
+/* Write every group's prompt K/V into its prefix pages. bf16 pools copy the
+ * rows. fp8 pools give each (page, kv-head) of a prompt, in fp32,
+ * scale = amax / 448 over the page's written rows (1.0 when amax = 0) and
+ * store e4m3(x / scale) (round to nearest even, saturating at 448); rows past
+ * a prompt's end are not written. k, v: bf16 [T][Hkv][head_dim], 16-byte
+ * aligned. Prompts must not share pages. */
+rp_status rp_prefill_kv_write(const rp_paged_kv* kv, const rp_prefill_layout* layout,
+                              const void* k, const void* v, hipStream_t stream);
+
+/* Causal attention within each prompt: for token t of group g and query head
+ * j (kv-head j / (Hq / Hkv)), over the group's tokens u <= t,
+ *   s_u = softmax_scale * <q_t[j], k_u>, lse = ln sum_u exp(s_u),
+ *   out[t][j] = sum_u exp(s_u - lse) v_u.
+ * Reads the bf16 projections q, k, v (not the pool; the pool only supplies
+ * Hkv and head_dim). out: bf16 [T][Hq][head_dim], 16-byte aligned; lse: fp32
+ * [T][Hq], natural log, may be NULL. */
+rp_status rp_prefill_attn(const rp_paged_kv* kv, const rp_prefill_layout* layout,
+                          const void* q, const void* k, const void* v, float softmax_scale,
+                          void* out, float* lse, hipStream_t stream);
+
 /* ---- Staged form of rp_group_decode_attn -------------------------------
  * A decode step's layout is shared by every layer, so a caller can plan once
  * and run the attention of all layers against the same plan. */

@@ -27,7 +27,8 @@ RP_KV_FP8_E4M3 = 1
 
 EXPORTED = ("rp_status_string", "rp_last_error", "rp_kv_append",
             "rp_group_decode_attn_workspace_size", "rp_group_decode_attn", "rp_lse_combine",
-            "rp_plan", "rp_attn_parts", "rp_combine_parts", "rp_plan_layout", "rp_validate_layout")
+            "rp_plan", "rp_attn_parts", "rp_combine_parts", "rp_plan_layout", "rp_validate_layout",
+            "rp_prefill_kv_write", "rp_prefill_attn")
 
 
 class RpPagedKV(ctypes.Structure):
@@ -45,6 +46,12 @@ class RpGroupLayout(ctypes.Structure):
                 ("prefix_block_table", ctypes.c_void_p), ("max_prefix_pages", ctypes.c_int32),
                 ("resp_lens", ctypes.c_void_p), ("resp_block_table", ctypes.c_void_p),
                 ("max_resp_pages", ctypes.c_int32)]
+
+
+class RpPrefillLayout(ctypes.Structure):
+    _fields_ = [("num_groups", ctypes.c_int32), ("num_q_heads", ctypes.c_int32), ("num_tokens", ctypes.c_int32),
+                ("prompt_offs", ctypes.c_void_p), ("prefix_block_table", ctypes.c_void_p),
+                ("max_prefix_pages", ctypes.c_int32)]
 
 
 class RpPlanInfo(ctypes.Structure):
@@ -83,6 +90,8 @@ def load() -> ctypes.CDLL:
         "rp_combine_parts": (ctypes.c_int, [P, P, P, P, P, ctypes.c_size_t, P]),
         "rp_plan_layout": (ctypes.c_int, [P, P, P]),
         "rp_validate_layout": (ctypes.c_int, [P, P, P]),
+        "rp_prefill_kv_write": (ctypes.c_int, [P, P, P, P, P]),
+        "rp_prefill_attn": (ctypes.c_int, [P, P, P, P, P, F32, P, P, P]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -203,3 +212,19 @@ def plan_layout(kv, layout) -> RpPlanInfo:
 def validate_layout(kv, layout, stream=None) -> None:
     _check(load().rp_validate_layout(ctypes.byref(kv), ctypes.byref(layout), _stream(stream)),
            "rp_validate_layout")
+
+
+def prefill_layout(prompt_offs, prefix_block_table, *, num_q_heads, num_tokens) -> RpPrefillLayout:
+    """Describe packed prompts: group g owns rows prompt_offs[g] .. prompt_offs[g+1]-1."""
+    return RpPrefillLayout(int(prompt_offs.shape[0]) - 1, int(num_q_heads), int(num_tokens), _ptr(prompt_offs),
+                           _ptr(prefix_block_table), int(prefix_block_table.shape[1]))
+
+
+def prefill_kv_write(kv, layout, k, v, stream=None) -> None:
+    _check(load().rp_prefill_kv_write(ctypes.byref(kv), ctypes.byref(layout), _ptr(k), _ptr(v), _stream(stream)),
+           "rp_prefill_kv_write")
+
+
+def prefill_attn(kv, layout, q, k, v, softmax_scale, out, lse, stream=None) -> None:
+    _check(load().rp_prefill_attn(ctypes.byref(kv), ctypes.byref(layout), _ptr(q), _ptr(k), _ptr(v),
+                                  float(softmax_scale), _ptr(out), _ptr(lse), _stream(stream)), "rp_prefill_attn")

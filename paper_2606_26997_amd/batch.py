@@ -123,3 +123,41 @@ class DeviceBatch:
 
     def validate(self, stream=None):
         B.validate_layout(self.kv, self.attn_layout, stream)
+
+
+class PrefillBatch:
+    """Packed prompts of several groups on the device, for the shared-prefix prefill."""
+
+    def __init__(self, *, q, k, v, prompt_offs, prefix_block_table, k_pages, v_pages, k_scale=None, v_scale=None,
+                 num_q_heads, softmax_scale, device="cuda"):
+        d = self.device = torch.device(device)
+        self.q, self.k, self.v = _dev(q, d), _dev(k, d), _dev(v, d)
+        self.prompt_offs = _dev(prompt_offs, d, torch.int32)
+        self.prefix_block_table = _dev(prefix_block_table, d, torch.int32)
+        self.k_pages, self.v_pages = _dev(k_pages, d), _dev(v_pages, d)
+        self.k_scale = _dev(k_scale, d, torch.float32)
+        self.v_scale = _dev(v_scale, d, torch.float32)
+        self.softmax_scale = float(softmax_scale)
+        T = int(self.q.shape[0])
+        self.out = torch.zeros((T, int(num_q_heads), int(self.q.shape[2])), dtype=torch.bfloat16, device=d)
+        self.lse = torch.zeros((T, int(num_q_heads)), dtype=torch.float32, device=d)
+        self.kv = B.paged_kv(self.k_pages, self.v_pages, self.k_scale, self.v_scale)
+        self.layout = B.prefill_layout(self.prompt_offs, self.prefix_block_table, num_q_heads=num_q_heads,
+                                       num_tokens=T)
+
+    @classmethod
+    def from_workload(cls, w, device="cuda"):
+        return cls(q=w.q, k=w.k, v=w.v, prompt_offs=w.prefix_offs, prefix_block_table=w.prefix_block_table,
+                   k_pages=w.k_pages, v_pages=w.v_pages, k_scale=w.k_scale, v_scale=w.v_scale,
+                   num_q_heads=w.num_q_heads, softmax_scale=w.softmax_scale, device=device)
+
+    def kv_write(self, stream=None):
+        B.prefill_kv_write(self.kv, self.layout, self.k, self.v, stream)
+
+    def attention(self, stream=None):
+        B.prefill_attn(self.kv, self.layout, self.q, self.k, self.v, self.softmax_scale, self.out, self.lse, stream)
+
+    def step(self, stream=None):
+        """Write the prompts' K/V pages, then attend within each prompt."""
+        self.kv_write(stream)
+        self.attention(stream)

@@ -11,7 +11,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "librp.so")
-SOURCES = ["rp_api.hip", "rp_plan.hip", "rp_attn.hip", "rp_combine.hip", "rp_append.hip"]
+SOURCES = ["rp_api.hip", "rp_plan.hip", "rp_attn.hip", "rp_combine.hip", "rp_append.hip", "rp_prefill.hip"]
 ARCH = "gfx950"
 
 # Packed-fp32 VALU instructions are disabled for all device code. MFMA

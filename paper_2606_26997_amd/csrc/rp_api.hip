@@ -345,6 +345,81 @@ rp_status rp_kv_append(const rp_paged_kv* kv, const rp_group_layout* l, const vo
   return e == hipSuccess ? RP_OK : hip_fail(e, "append kernel launch");
 }
 
+// Shared checks of the prefill calls; fills a (pointers of the projections
+// and outputs are checked by the callers).
+static rp_status prefill_args(const rp_paged_kv* kv, const rp_prefill_layout* l, rp::PrefillArgs* a, int* n_rep) {
+  rp_status st = check_kv(kv);
+  if (st != RP_OK) return st;
+  if (l == nullptr) return fail(RP_ERR_INVALID_ARG, "layout is NULL");
+  if (l->num_groups < 0 || l->num_tokens < 0) return fail(RP_ERR_INVALID_ARG, "num_groups/num_tokens must be >= 0");
+  if (l->num_q_heads < 1 || l->num_q_heads % kv->num_kv_heads != 0)
+    return fail(RP_ERR_INVALID_ARG, "num_q_heads %d not a positive multiple of num_kv_heads %d", l->num_q_heads,
+                kv->num_kv_heads);
+  const int r = l->num_q_heads / kv->num_kv_heads;
+  if (r != 1 && r != 2 && r != 4 && r != 8)
+    return fail(RP_ERR_UNSUPPORTED, "q/kv head ratio %d unsupported (1, 2, 4, 8)", r);
+  if (l->num_groups > 0) {
+    if (l->prompt_offs == nullptr) return fail(RP_ERR_INVALID_ARG, "prompt_offs is NULL");
+    if (l->max_prefix_pages < 1 || l->prefix_block_table == nullptr)
+      return fail(RP_ERR_INVALID_ARG, "prefix_block_table must be non-NULL with max_prefix_pages >= 1");
+  }
+  if ((long long)l->num_groups * l->max_prefix_pages * kv->num_kv_heads >= (1ll << 31) ||
+      (long long)l->num_tokens * l->num_q_heads * kv->head_dim >= (1ll << 40))
+    return fail(RP_ERR_UNSUPPORTED, "prefill too large");
+  a->k_pages = kv->k_pages;
+  a->v_pages = kv->v_pages;
+  a->k_scale = kv->k_scale;
+  a->v_scale = kv->v_scale;
+  a->num_pages = kv->num_pages;
+  a->num_kv_heads = kv->num_kv_heads;
+  a->num_groups = l->num_groups;
+  a->num_q_heads = l->num_q_heads;
+  a->num_tokens = l->num_tokens;
+  a->prompt_offs = l->prompt_offs;
+  a->prefix_block_table = l->prefix_block_table;
+  a->max_prefix_pages = l->max_prefix_pages;
+  *n_rep = r;
+  return RP_OK;
+}
+
+rp_status rp_prefill_kv_write(const rp_paged_kv* kv, const rp_prefill_layout* l, const void* k, const void* v,
+                              hipStream_t stream) {
+  g_err[0] = 0;
+  rp::PrefillArgs a{};
+  int n_rep = 0;
+  rp_status st = prefill_args(kv, l, &a, &n_rep);
+  if (st != RP_OK) return st;
+  if (l->num_groups == 0 || l->num_tokens == 0) return RP_OK;
+  if (k == nullptr || v == nullptr || !aligned(k, 16) || !aligned(v, 16))
+    return fail(RP_ERR_INVALID_ARG, "k/v must be non-NULL and 16-byte aligned");
+  a.k = k;
+  a.v = v;
+  hipError_t e = rp::launch_prefill_kv_write(a, kv->head_dim, kv->kv_dtype == RP_KV_FP8_E4M3, stream);
+  return e == hipSuccess ? RP_OK : hip_fail(e, "prefill KV write kernel launch");
+}
+
+rp_status rp_prefill_attn(const rp_paged_kv* kv, const rp_prefill_layout* l, const void* q, const void* k,
+                          const void* v, float softmax_scale, void* out, float* lse, hipStream_t stream) {
+  g_err[0] = 0;
+  rp::PrefillArgs a{};
+  int n_rep = 0;
+  rp_status st = prefill_args(kv, l, &a, &n_rep);
+  if (st != RP_OK) return st;
+  if (l->num_groups == 0 || l->num_tokens == 0) return RP_OK;
+  if (q == nullptr || k == nullptr || v == nullptr || !aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16))
+    return fail(RP_ERR_INVALID_ARG, "q/k/v must be non-NULL and 16-byte aligned");
+  if (out == nullptr || !aligned(out, 16)) return fail(RP_ERR_INVALID_ARG, "out must be non-NULL and 16-byte aligned");
+  if (lse != nullptr && !aligned(lse, 4)) return fail(RP_ERR_INVALID_ARG, "lse must be 4-byte aligned");
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.qk_scale = softmax_scale * rp::kLog2e;
+  a.out = out;
+  a.lse = lse;
+  hipError_t e = rp::launch_prefill_attn(a, kv->head_dim, n_rep, stream);
+  return e == hipSuccess ? RP_OK : hip_fail(e, "prefill attention kernel launch");
+}
+
 rp_status rp_plan_layout(const rp_paged_kv* kv, const rp_group_layout* l, rp_plan_info* info) {
   g_err[0] = 0;
   if (info == nullptr) return fail(RP_ERR_INVALID_ARG, "info is NULL");

@@ -139,14 +139,6 @@ __device__ inline size_t resp_block(const AttnArgs& a, int page, int h, int lane
 // ---------------------------------------------------------------------------
 // Group-prefix path
 // ---------------------------------------------------------------------------
-__device__ inline f32x4_t mfma16x16x32(const bf16x8_t& a, const bf16x8_t& b, const f32x4_t& c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
-}
-__device__ inline f32x4_t mfma16x16x16(const bf16x4_t& a, const bf16x4_t& b, const f32x4_t& c) {
-  typedef short s16x4_t __attribute__((ext_vector_type(4)));
-  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4_t, a), __builtin_bit_cast(s16x4_t, b),
-                                                   c, 0, 0, 0);
-}
 
 // One page of a prefix unit in flight, as loaded (this lane's share):
 //  k: the A operand of S^T = K Q^T, lane (r16, quad) holds

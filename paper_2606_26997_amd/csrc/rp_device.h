@@ -150,6 +150,19 @@ __device__ inline float xor_sum_from(float x) {
   return x;
 }
 
+// MFMA tiles used by the group-prefix and prefill paths (fp32 accumulate):
+//   16x16x32 bf16: lane (r, q) supplies A[r][8q..8q+7] and B[8q..8q+7][r];
+//   16x16x16 bf16: lane (r, q) supplies A[r][4q..4q+3] and B[4q..4q+3][r];
+// lane (r, q) receives C[4q..4q+3][r].
+__device__ inline f32x4_t mfma16x16x32(const bf16x8_t& a, const bf16x8_t& b, const f32x4_t& c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+__device__ inline f32x4_t mfma16x16x16(const bf16x4_t& a, const bf16x4_t& b, const f32x4_t& c) {
+  typedef short s16x4_t __attribute__((ext_vector_type(4)));
+  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4_t, a), __builtin_bit_cast(s16x4_t, b),
+                                                   c, 0, 0, 0);
+}
+
 __device__ inline float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ inline float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
 

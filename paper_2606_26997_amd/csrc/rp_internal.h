@@ -78,6 +78,26 @@ struct AppendArgs {
   const void* v_new;
 };
 
+// Shared-prefix prefill: packed prompt tokens of every group (group g owns
+// rows prompt_offs[g] .. prompt_offs[g+1]-1 of q/k/v/out), K/V written once
+// into the group's prefix pages.
+struct PrefillArgs {
+  void* k_pages;
+  void* v_pages;
+  float* k_scale;
+  float* v_scale;
+  int num_pages, num_kv_heads, num_groups, num_q_heads, num_tokens;
+  const int* prompt_offs;
+  const int* prefix_block_table;
+  int max_prefix_pages;
+  const void* q;  // bf16 [T][Hq][D]
+  const void* k;  // bf16 [T][Hkv][D]
+  const void* v;
+  float qk_scale;  // softmax_scale * log2(e)
+  void* out;       // bf16 [T][Hq][D]
+  float* lse;      // [T][Hq] or null
+};
+
 struct ValidateArgs {
   int num_pages, num_seqs, num_groups;
   const int* seq_to_group;
@@ -96,6 +116,8 @@ hipError_t launch_attn_parts(const AttnArgs& a, int head_dim, int n_rep, bool fp
                              long long max_resp_items, hipStream_t stream);
 hipError_t launch_combine(const CombineArgs& a, int head_dim, hipStream_t stream);
 hipError_t launch_append(const AppendArgs& a, int head_dim, bool fp8, hipStream_t stream);
+hipError_t launch_prefill_kv_write(const PrefillArgs& a, int head_dim, bool fp8, hipStream_t stream);
+hipError_t launch_prefill_attn(const PrefillArgs& a, int head_dim, int n_rep, hipStream_t stream);
 hipError_t launch_validate(const ValidateArgs& a, hipStream_t stream);
 
 }  // namespace rp

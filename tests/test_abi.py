@@ -169,3 +169,36 @@ def test_plan_layout_sections_fit_the_workspace():
     assert info.part_o + 4 * info.max_parts * 64 <= info.part_lse
     with pytest.raises(B.RpError):
         B.plan_layout(_kv(head_dim=96), lay)
+
+
+def _prefill_layout(**kw):
+    d = dict(num_groups=2, num_q_heads=4, num_tokens=10, offs=A, pbt=A, mpp=2)
+    d.update(kw)
+    return B.RpPrefillLayout(d["num_groups"], d["num_q_heads"], d["num_tokens"], d["offs"], d["pbt"], d["mpp"])
+
+
+@pytest.mark.parametrize("lay_kw,status,needle", [
+    (dict(num_q_heads=3), rp.RP_ERR_INVALID_ARG, "multiple"),
+    (dict(num_q_heads=6), rp.RP_ERR_UNSUPPORTED, "ratio"),
+    (dict(offs=None), rp.RP_ERR_INVALID_ARG, "prompt_offs"),
+    (dict(mpp=0), rp.RP_ERR_INVALID_ARG, "max_prefix_pages"),
+    (dict(num_tokens=-1), rp.RP_ERR_INVALID_ARG, "num_tokens"),
+])
+def test_prefill_layout_checks(lay_kw, status, needle):
+    lib = rp.load()
+    st = lib.rp_prefill_kv_write(ctypes.byref(_kv()), ctypes.byref(_prefill_layout(**lay_kw)), A, A, None)
+    assert st == status and needle in rp.last_error()
+
+
+def test_prefill_pointer_checks():
+    lib = rp.load()
+    kv, lay = _kv(), _prefill_layout()
+    assert lib.rp_prefill_kv_write(ctypes.byref(kv), ctypes.byref(lay), None, A, None) == rp.RP_ERR_INVALID_ARG
+    assert lib.rp_prefill_kv_write(ctypes.byref(kv), ctypes.byref(lay), A + 2, A, None) == rp.RP_ERR_INVALID_ARG
+    st = lib.rp_prefill_attn(ctypes.byref(kv), ctypes.byref(lay), A, A, A, ctypes.c_float(0.1), None, None, None)
+    assert st == rp.RP_ERR_INVALID_ARG and "out" in rp.last_error()
+    st = lib.rp_prefill_attn(ctypes.byref(kv), ctypes.byref(lay), A, A, A, ctypes.c_float(0.1), A, A + 2, None)
+    assert st == rp.RP_ERR_INVALID_ARG and "lse" in rp.last_error()
+    # Nothing to do: returns before touching any pointer.
+    assert lib.rp_prefill_attn(ctypes.byref(kv), ctypes.byref(_prefill_layout(num_tokens=0)), None, None, None,
+                               ctypes.c_float(0.1), None, None, None) == rp.RP_OK
