@@ -46,6 +46,11 @@ def parse_args():
                    help="wall-clock budget of the oracle CPU baseline sample (0 disables it)")
     p.add_argument("--copy-calibration", action="store_true",
                    help="run only a plain device copy of known size (for HBM counter scaling)")
+    p.add_argument("--prefill", action="store_true",
+                   help="time the shared-prefix prefill (one prompt per group: K/V page write + causal "
+                        "attention) on the workload's prompts instead of the decode step")
+    p.add_argument("--prefill-len", type=int, default=None,
+                   help="with --prefill: every prompt this many tokens instead of the workload's lengths")
     p.add_argument("--traffic-from", metavar="DIR", default=None,
                    help="summarise rocprofv3 --pmc runs under DIR (pmc_fetch, pmc_write, pmc_copy_fetch, "
                         "pmc_copy_write) into the stored HBM traffic of the partial-attention kernel")
@@ -182,6 +187,68 @@ def copy_calibration(steps):
                       "GBps_read_plus_write": 2 * n / el / 1e9}), flush=True)
 
 
+def prefill_bench(args):
+    """Shared-prefix prefill: per step, every group's prompt K/V written once and causal attention."""
+    import numpy as np
+    import torch
+    import paper_2606_26997_amd as rp
+    from workloads import CONFIGS, make_prefill_workload
+
+    cfg = CONFIGS[args.config]
+    rng = np.random.default_rng(cfg.seed if args.seed is None else args.seed)
+    if args.prefill_len is not None:
+        P = np.full(cfg.groups, args.prefill_len)
+    elif cfg.prefix[0] == "fixed":
+        P = np.full(cfg.groups, cfg.prefix[1])
+    else:
+        P = rng.integers(cfg.prefix[1], cfg.prefix[2] + 1, cfg.groups)
+    w = make_prefill_workload(num_q_heads=cfg.num_q_heads, num_kv_heads=cfg.num_kv_heads, head_dim=cfg.head_dim,
+                              prefix_lens=P, seed=cfg.seed, kv_dtype=cfg.kv_dtype, k_mult=cfg.k_mult)
+    torch.cuda.set_device(0)
+    b = rp.PrefillBatch.from_workload(w, device="cuda:0")
+    T, Hq, Hkv, d = w.num_tokens, w.num_q_heads, w.num_kv_heads, w.head_dim
+    eb = 1 if w.kv_dtype == "fp8" else 2
+    P64 = P.astype(np.int64)
+    # Algorithmic bytes: q, k, v read once, out written, K/V pages written (+ fp8 scales), lse.
+    nbytes = T * (Hq + 2 * Hkv + Hq) * d * 2 + T * Hkv * d * 2 * eb + T * Hq * 4
+    if w.kv_dtype == "fp8":
+        nbytes += int(((P64 + 15) // 16).sum()) * Hkv * 8
+    # Causal attention flops: QK and PV over the u <= t pairs (2 flops per multiply-add).
+    flops = int((P64 * (P64 + 1) // 2).sum()) * Hq * d * 4
+    for _ in range(args.warmup):
+        b.step()
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        b.kv_write()
+        ev[k][0].record()
+        b.attention()
+        ev[k][1].record()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) / args.steps * 1e3
+    attn_us = float(np.mean([a.elapsed_time(c) for a, c in ev])) * 1e3
+    attn_bytes = T * (Hq + 2 * Hkv + Hq) * d * 2 + T * Hq * 4
+    line = {
+        "metric": "shared-prefix prefill: prompt tokens/s and achieved HBM GB/s (one prompt per group)",
+        "value": round(T / (ms * 1e-3), 1), "unit": "prompt tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"config{cfg.cid} prompts" + (f" of {args.prefill_len} tokens" if args.prefill_len else ""),
+                   "groups": int(cfg.groups), "prompt_tokens": T, "q_heads": Hq, "kv_heads": Hkv, "head_dim": d,
+                   "kv_dtype": w.kv_dtype},
+        "GBps": round(nbytes / (ms * 1e-3) / 1e9, 1), "attn_tflops": round(flops / (attn_us * 1e-6) / 1e12, 2),
+        "attn_us": round(attn_us, 2),
+        "roofline": {"kernel": "prefill_attn_kernel", "bound": "hbm" if flops / attn_bytes < 310 else "mfma",
+                     "achieved": round(attn_bytes / (attn_us * 1e-6) / 1e9, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(attn_bytes / (attn_us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "algorithmic_bytes_per_launch": int(attn_bytes), "flops_per_launch": flops,
+                     "mfma_frac": round(flops / (attn_us * 1e-6) / 2.5e15, 4)},
+        "cpu_baseline": None,
+    }
+    print(json.dumps(line), flush=True)
+
+
 def main():
     args = parse_args()
     if args.gpus != 1:
@@ -197,6 +264,9 @@ def main():
         return
     if args.traffic_from:
         summarise_traffic(args.traffic_from)
+        return
+    if args.prefill:
+        prefill_bench(args)
         return
 
     import paper_2606_26997_amd as rp
