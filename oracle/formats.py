@@ -58,3 +58,22 @@ def e4m3_encode(x) -> np.ndarray:
     code = np.where(exact, hi, np.where(pick_hi, hi, lo))
     code = np.where(a >= E4M3_MAX, 126, code)
     return (code.astype(np.uint8) | (sign << np.uint8(7))).astype(np.uint8)
+
+
+def f64_to_bf16_bits(x) -> np.ndarray:
+    """Round float64 values to bf16 (nearest, ties to even) in one step; bit patterns as uint16.
+
+    A bf16 value is a multiple of ulp = 2^(e - 7) where 2^e <= |x| < 2^(e+1)
+    (e clamped at -126 below, the subnormal range); |x| / ulp < 2^8, so the
+    rounding of that quotient in float64 is exact. Finite inputs only.
+    """
+    x = np.asarray(x, dtype=np.float64)
+    if not np.isfinite(x).all():
+        raise ValueError("f64_to_bf16_bits: non-finite input")
+    a = np.abs(x)
+    _, e = np.frexp(a)                     # a = f * 2^e with 0.5 <= f < 1, so 2^(e-1) <= a
+    e = np.maximum(e - 1, -126)
+    ulp = np.ldexp(1.0, e - 7)
+    r = np.rint(a / ulp) * ulp             # np.rint rounds half to even
+    v = np.where(np.signbit(x), -r, r).astype(np.float32)   # exact: r is a bf16 value
+    return (v.view(np.uint32) >> np.uint32(16)).astype(np.uint16)

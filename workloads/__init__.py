@@ -7,6 +7,8 @@ attention arithmetic, so it can be shared by both sides without coupling them.
 from .configs import CONFIGS, config_by_id
 from .gen import Workload, make_config_workload, make_workload
 from .prefill import PrefillWorkload, make_prefill_workload
+from .qkprep import QkPrepInputs, make_qkprep_inputs
 
 __all__ = ["CONFIGS", "config_by_id", "Workload", "make_config_workload", "make_workload",
-           "PrefillWorkload", "make_prefill_workload"]
+           "PrefillWorkload", "make_prefill_workload",
+           "QkPrepInputs", "make_qkprep_inputs"]
