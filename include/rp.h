@@ -120,6 +120,34 @@ const char* rp_last_error(void);
 rp_status rp_kv_append(const rp_paged_kv* kv, const rp_group_layout* layout,
                        const void* k_new, const void* v_new, hipStream_t stream);
 
+/* Pre-attention side of one decode step of a Qwen3-style attention layer
+ * (the paper's policy model, Section 5.1): RMS norm of every q and k head
+ * with the layer's per-channel weights, then the rotary position embedding,
+ * then the append of k and v.
+ * The new token of sequence s (group g = seq_to_group[s]) is at position
+ * p_s = prefix_lens[g] + resp_lens[s]. For a head vector x of head_dim d,
+ *   y = x / sqrt(mean(x^2) + rms_eps) * w,
+ *   out[i]       = y[i] cos(a_i) - y[i + d/2] sin(a_i),
+ *   out[i + d/2] = y[i + d/2] cos(a_i) + y[i] sin(a_i),  a_i = p_s * rope_theta^(-2i/d),
+ * for i < d/2, with w = q_norm_w for q heads and k_norm_w for k heads.
+ * Computed in fp64 from the bf16 inputs and rounded once to bf16 (nearest
+ * even): outputs equal the correctly rounded values except where the exact
+ * value lies within a few fp64 ulps of a rounding boundary (then they are
+ * one bf16 ulp away).
+ * q_in: bf16 [S][Hq][d]; k_in, v_in: bf16 [S][Hkv][d]; q_norm_w, k_norm_w:
+ * bf16 [d]; q_out: bf16 [S][Hq][d] (the q layout rp_group_decode_attn reads),
+ * may be q_in itself but must not otherwise overlap it; k_out: bf16
+ * [S][Hkv][d] copy of the rotated k, or NULL. The rotated k and the
+ * unchanged v are appended exactly as rp_kv_append would append them (same
+ * slot, same fp8 rule); a sequence with resp_lens[s] outside
+ * [0, max_resp_pages * 16) gets q_out (and k_out) but no append. rms_eps must
+ * be finite and >= 0 (Qwen3: 1e-6), rope_theta finite and > 0 (Qwen3: 1e6). */
+rp_status rp_decode_qk_prep(const rp_paged_kv* kv, const rp_group_layout* layout,
+                            const void* q_in, const void* k_in, const void* v_in,
+                            const void* q_norm_w, const void* k_norm_w,
+                            double rms_eps, double rope_theta,
+                            void* q_out, void* k_out, hipStream_t stream);
+
 /* Workspace bytes needed by rp_group_decode_attn / rp_plan for this shape.
  * Depends only on host-side scalars (S, num_groups, Hq, Hkv, head_dim,
  * max_prefix_pages, max_resp_pages); *bytes is a host pointer. */

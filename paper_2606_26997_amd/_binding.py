@@ -28,7 +28,7 @@ RP_KV_FP8_E4M3 = 1
 EXPORTED = ("rp_status_string", "rp_last_error", "rp_kv_append",
             "rp_group_decode_attn_workspace_size", "rp_group_decode_attn", "rp_lse_combine",
             "rp_plan", "rp_attn_parts", "rp_combine_parts", "rp_plan_layout", "rp_validate_layout",
-            "rp_prefill_kv_write", "rp_prefill_attn")
+            "rp_prefill_kv_write", "rp_prefill_attn", "rp_decode_qk_prep")
 
 
 class RpPagedKV(ctypes.Structure):
@@ -92,6 +92,7 @@ def load() -> ctypes.CDLL:
         "rp_validate_layout": (ctypes.c_int, [P, P, P]),
         "rp_prefill_kv_write": (ctypes.c_int, [P, P, P, P, P]),
         "rp_prefill_attn": (ctypes.c_int, [P, P, P, P, P, F32, P, P, P]),
+        "rp_decode_qk_prep": (ctypes.c_int, [P, P, P, P, P, P, P, ctypes.c_double, ctypes.c_double, P, P, P]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -156,6 +157,14 @@ def group_layout(seq_to_group, prefix_lens, prefix_block_table, resp_lens, resp_
 def kv_append(kv: RpPagedKV, layout: RpGroupLayout, k_new, v_new, stream=None) -> None:
     _check(load().rp_kv_append(ctypes.byref(kv), ctypes.byref(layout), _ptr(k_new), _ptr(v_new),
                                _stream(stream)), "rp_kv_append")
+
+
+def decode_qk_prep(kv, layout, q_in, k_in, v_in, q_norm_w, k_norm_w, q_out, k_out=None, *,
+                   rms_eps=1e-6, rope_theta=1e6, stream=None) -> None:
+    _check(load().rp_decode_qk_prep(ctypes.byref(kv), ctypes.byref(layout), _ptr(q_in), _ptr(k_in), _ptr(v_in),
+                                    _ptr(q_norm_w), _ptr(k_norm_w), float(rms_eps), float(rope_theta),
+                                    _ptr(q_out), _ptr(k_out), _stream(stream)),
+           "rp_decode_qk_prep")
 
 
 def group_decode_attn_workspace_size(kv: RpPagedKV, layout: RpGroupLayout) -> int:

@@ -95,6 +95,29 @@ class DeviceBatch:
             self.kv_append(stream)
         self.attention(stream)
 
+    # -- decode step from the raw projections ---------------------------------
+    def set_projections(self, q_in, k_in, v_in, q_norm_w, k_norm_w, *, rms_eps=1e-6, rope_theta=1e6,
+                        keep_k=False):
+        """Raw (pre-norm) projections of the new token; ``decode_step`` then builds q and the appended k/v."""
+        if not self.append:
+            raise ValueError("set_projections needs a batch built with append=True")
+        d = self.device
+        self.q_in, self.k_in, self.v_in = _dev(q_in, d), _dev(k_in, d), _dev(v_in, d)
+        self.q_norm_w, self.k_norm_w = _dev(q_norm_w, d), _dev(k_norm_w, d)
+        self.rms_eps, self.rope_theta = float(rms_eps), float(rope_theta)
+        self.k_out = torch.empty_like(self.k_in) if keep_k else None
+
+    def qk_prep(self, stream=None):
+        """RMS norm + rotary embedding of q (into ``self.q``) and k, and the append of k and v."""
+        B.decode_qk_prep(self.kv, self.append_layout, self.q_in, self.k_in, self.v_in, self.q_norm_w,
+                         self.k_norm_w, self.q, self.k_out, rms_eps=self.rms_eps, rope_theta=self.rope_theta,
+                         stream=stream)
+
+    def decode_step(self, stream=None):
+        """Pre-attention prep (with the append), then attention over the advanced lengths."""
+        self.qk_prep(stream)
+        self.attention(stream)
+
     # -- staged form ------------------------------------------------------------
     def plan(self, stream=None):
         B.plan(self.kv, self.attn_layout, self.workspace, stream)

@@ -11,7 +11,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "librp.so")
-SOURCES = ["rp_api.hip", "rp_plan.hip", "rp_attn.hip", "rp_combine.hip", "rp_append.hip", "rp_prefill.hip"]
+SOURCES = ["rp_api.hip", "rp_plan.hip", "rp_attn.hip", "rp_combine.hip", "rp_append.hip", "rp_prefill.hip",
+           "rp_qkprep.hip"]
 ARCH = "gfx950"
 
 # Packed-fp32 VALU instructions are disabled for all device code. MFMA

@@ -1,6 +1,7 @@
 // C-ABI entry points: argument validation, workspace layout and kernel
 // launches on the caller's stream. No device allocation and no host sync on
 // the hot path; rp_validate_layout is the one test utility that does both.
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -343,6 +344,52 @@ rp_status rp_kv_append(const rp_paged_kv* kv, const rp_group_layout* l, const vo
   a.v_new = v_new;
   hipError_t e = rp::launch_append(a, sh.D, sh.fp8, stream);
   return e == hipSuccess ? RP_OK : hip_fail(e, "append kernel launch");
+}
+
+rp_status rp_decode_qk_prep(const rp_paged_kv* kv, const rp_group_layout* l, const void* q_in, const void* k_in,
+                            const void* v_in, const void* q_norm_w, const void* k_norm_w, double rms_eps,
+                            double rope_theta, void* q_out, void* k_out, hipStream_t stream) {
+  g_err[0] = 0;
+  Shape sh;
+  rp_status st = check_shape(kv, l, &sh);
+  if (st != RP_OK) return st;
+  if (!(rms_eps >= 0.0) || !std::isfinite(rms_eps)) return fail(RP_ERR_INVALID_ARG, "rms_eps must be finite and >= 0");
+  if (!(rope_theta > 0.0) || !std::isfinite(rope_theta))
+    return fail(RP_ERR_INVALID_ARG, "rope_theta must be finite and > 0");
+  if (sh.S == 0) return RP_OK;
+  const void* in[] = {q_in, k_in, v_in, q_norm_w, k_norm_w, q_out};
+  for (const void* p : in)
+    if (p == nullptr || !aligned(p, 2))
+      return fail(RP_ERR_INVALID_ARG, "q_in/k_in/v_in/q_norm_w/k_norm_w/q_out must be non-NULL bf16 arrays");
+  if (k_out != nullptr && !aligned(k_out, 2)) return fail(RP_ERR_INVALID_ARG, "k_out must be a bf16 array");
+  if (sh.max_rp < 1) return fail(RP_ERR_INVALID_ARG, "max_resp_pages must be >= 1 to append");
+  rp::QkPrepArgs a;
+  a.k_pages = kv->k_pages;
+  a.v_pages = kv->v_pages;
+  a.k_scale = kv->k_scale;
+  a.v_scale = kv->v_scale;
+  a.num_pages = kv->num_pages;
+  a.num_kv_heads = sh.Hkv;
+  a.num_q_heads = sh.Hq;
+  a.num_seqs = sh.S;
+  a.num_groups = sh.G;
+  a.seq_to_group = l->seq_to_group;
+  a.prefix_lens = l->prefix_lens;
+  a.resp_lens = l->resp_lens;
+  a.resp_block_table = l->resp_block_table;
+  a.max_resp_pages = sh.max_rp;
+  a.q_in = static_cast<const uint16_t*>(q_in);
+  a.k_in = static_cast<const uint16_t*>(k_in);
+  a.v_in = static_cast<const uint16_t*>(v_in);
+  a.q_norm_w = static_cast<const uint16_t*>(q_norm_w);
+  a.k_norm_w = static_cast<const uint16_t*>(k_norm_w);
+  a.rms_eps = rms_eps;
+  a.rope_theta = rope_theta;
+  a.q_out = static_cast<uint16_t*>(q_out);
+  a.k_out = static_cast<uint16_t*>(k_out);
+  a.blocks_per_seq = a.heads_per_block = 0;
+  hipError_t e = rp::launch_qk_prep(a, sh.D, sh.fp8, stream);
+  return e == hipSuccess ? RP_OK : hip_fail(e, "decode q/k prep kernel launch");
 }
 
 // Shared checks of the prefill calls; fills a (pointers of the projections

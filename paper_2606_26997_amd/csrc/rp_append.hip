@@ -1,11 +1,7 @@
 // KV append: one wave per (sequence, kv-head) writes the new token into
 // response slot L = resp_lens[s] (page resp_block_table[s][L / 16], row L % 16).
-// bf16 pools copy the values. fp8 pools quantise with the per-(page, kv-head)
-// scale rule: row 0 sets scale = amax / 448; a later row keeps the scale when
-// amax <= 448 * scale, and otherwise raises it to amax / 448 after
-// requantising rows 0..r-1 from code * old_scale. All of it is plain IEEE fp32
-// (no contraction, correctly rounded division), so the bytes written are a
-// deterministic function of the inputs.
+// bf16 pools copy the values; fp8 pools apply the per-(page, kv-head) scale
+// rule of append_fp8_row. Lane l handles columns l + 64 e.
 #include "rp_device.h"
 #include "rp_internal.h"
 
@@ -13,40 +9,6 @@
 
 namespace rp {
 namespace {
-
-template <int D>
-__device__ void append_fp8_head(uint8_t* blk, float* scale_slot, int r, const uint16_t* x_bits, int lane) {
-  constexpr int EPL = D / 64;
-  float x[EPL];
-  float amax = 0.f;
-#pragma unroll
-  for (int e = 0; e < EPL; ++e) {
-    x[e] = __uint_as_float((uint32_t)x_bits[lane * EPL + e] << 16);
-    amax = fmaxf(amax, fabsf(x[e]));
-  }
-  amax = xor_max_from<1>(amax);
-  const float old = *scale_slot;
-  float scale;
-  if (r == 0) {
-    scale = amax > 0.f ? amax / 448.0f : 1.0f;
-  } else if (amax <= 448.0f * old) {
-    scale = old;
-  } else {
-    scale = amax / 448.0f;
-    for (int rr = 0; rr < r; ++rr) {
-      uint8_t* row = blk + (size_t)rr * D + lane * EPL;
-#pragma unroll
-      for (int e = 0; e < EPL; ++e) {
-        const float val = e4m3_to_f32(row[e]) * old;
-        row[e] = (uint8_t)f32_to_e4m3(val / scale);
-      }
-    }
-  }
-  uint8_t* row = blk + (size_t)r * D + lane * EPL;
-#pragma unroll
-  for (int e = 0; e < EPL; ++e) row[e] = (uint8_t)f32_to_e4m3(x[e] / scale);
-  if (lane == 0) *scale_slot = scale;
-}
 
 template <int D, bool FP8>
 __global__ __launch_bounds__(64) void append_kernel(const AppendArgs a) {
@@ -64,17 +26,23 @@ __global__ __launch_bounds__(64) void append_kernel(const AppendArgs a) {
   const uint16_t* vn = static_cast<const uint16_t*>(a.v_new) + head_off;
   const size_t blk = ((size_t)page * Hkv + h) * kPage * D;  // in elements
   if constexpr (!FP8) {
-    uint16_t* kd = static_cast<uint16_t*>(a.k_pages) + blk + (size_t)r * D + lane * EPL;
-    uint16_t* vd = static_cast<uint16_t*>(a.v_pages) + blk + (size_t)r * D + lane * EPL;
+    uint16_t* kd = static_cast<uint16_t*>(a.k_pages) + blk + (size_t)r * D + lane;
+    uint16_t* vd = static_cast<uint16_t*>(a.v_pages) + blk + (size_t)r * D + lane;
 #pragma unroll
     for (int e = 0; e < EPL; ++e) {
-      kd[e] = kn[lane * EPL + e];
-      vd[e] = vn[lane * EPL + e];
+      kd[64 * e] = kn[64 * e + lane];
+      vd[64 * e] = vn[64 * e + lane];
     }
   } else {
     const size_t sidx = (size_t)page * Hkv + h;
-    append_fp8_head<D>(static_cast<uint8_t*>(a.k_pages) + blk, a.k_scale + sidx, r, kn, lane);
-    append_fp8_head<D>(static_cast<uint8_t*>(a.v_pages) + blk, a.v_scale + sidx, r, vn, lane);
+    float kx[EPL], vx[EPL];
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) {
+      kx[e] = __uint_as_float((uint32_t)kn[64 * e + lane] << 16);
+      vx[e] = __uint_as_float((uint32_t)vn[64 * e + lane] << 16);
+    }
+    append_fp8_row<D>(static_cast<uint8_t*>(a.k_pages) + blk, a.k_scale + sidx, r, kx, lane);
+    append_fp8_row<D>(static_cast<uint8_t*>(a.v_pages) + blk, a.v_scale + sidx, r, vx, lane);
   }
 }
 

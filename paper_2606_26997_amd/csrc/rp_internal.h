@@ -78,6 +78,30 @@ struct AppendArgs {
   const void* v_new;
 };
 
+// Pre-attention side of a decode step: q/k RMS norm + rotary embedding,
+// q written out, k and v appended at response slot resp_lens[s].
+struct QkPrepArgs {
+  void* k_pages;
+  void* v_pages;
+  float* k_scale;
+  float* v_scale;
+  int num_pages, num_kv_heads, num_q_heads, num_seqs, num_groups;
+  const int* seq_to_group;
+  const int* prefix_lens;
+  const int* resp_lens;
+  const int* resp_block_table;
+  int max_resp_pages;
+  const uint16_t* q_in;      // bf16 [S][Hq][D]
+  const uint16_t* k_in;      // bf16 [S][Hkv][D]
+  const uint16_t* v_in;
+  const uint16_t* q_norm_w;  // bf16 [D]
+  const uint16_t* k_norm_w;
+  double rms_eps, rope_theta;
+  uint16_t* q_out;           // bf16 [S][Hq][D]
+  uint16_t* k_out;           // bf16 [S][Hkv][D] or null
+  int blocks_per_seq, heads_per_block;  // set by the launcher
+};
+
 // Shared-prefix prefill: packed prompt tokens of every group (group g owns
 // rows prompt_offs[g] .. prompt_offs[g+1]-1 of q/k/v/out), K/V written once
 // into the group's prefix pages.
@@ -118,6 +142,7 @@ hipError_t launch_combine(const CombineArgs& a, int head_dim, hipStream_t stream
 hipError_t launch_append(const AppendArgs& a, int head_dim, bool fp8, hipStream_t stream);
 hipError_t launch_prefill_kv_write(const PrefillArgs& a, int head_dim, bool fp8, hipStream_t stream);
 hipError_t launch_prefill_attn(const PrefillArgs& a, int head_dim, int n_rep, hipStream_t stream);
+hipError_t launch_qk_prep(QkPrepArgs a, int head_dim, bool fp8, hipStream_t stream);
 hipError_t launch_validate(const ValidateArgs& a, hipStream_t stream);
 
 }  // namespace rp

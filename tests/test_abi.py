@@ -202,3 +202,22 @@ def test_prefill_pointer_checks():
     # Nothing to do: returns before touching any pointer.
     assert lib.rp_prefill_attn(ctypes.byref(kv), ctypes.byref(_prefill_layout(num_tokens=0)), None, None, None,
                                ctypes.c_float(0.1), None, None, None) == rp.RP_OK
+
+
+def test_decode_qk_prep_argument_checks():
+    kv, lay = _kv(), _layout()
+    lib = rp.load()
+    call = lambda kv_, lay_, q=A, k=A, v=A, wq=A, wk=A, eps=1e-6, theta=1e6, qo=A, ko=None: \
+        lib.rp_decode_qk_prep(ctypes.byref(kv_), ctypes.byref(lay_), q, k, v, wq, wk, eps, theta, qo, ko, None)
+    assert call(kv, lay, q=None) == rp.RP_ERR_INVALID_ARG and "q_in" in rp.last_error()
+    assert call(kv, lay, wk=None) == rp.RP_ERR_INVALID_ARG
+    assert call(kv, lay, qo=A + 1) == rp.RP_ERR_INVALID_ARG
+    assert call(kv, lay, ko=A + 1) == rp.RP_ERR_INVALID_ARG and "k_out" in rp.last_error()
+    assert call(kv, lay, eps=-1.0) == rp.RP_ERR_INVALID_ARG and "rms_eps" in rp.last_error()
+    assert call(kv, lay, eps=float("nan")) == rp.RP_ERR_INVALID_ARG
+    assert call(kv, lay, theta=0.0) == rp.RP_ERR_INVALID_ARG and "rope_theta" in rp.last_error()
+    assert call(kv, lay, theta=float("inf")) == rp.RP_ERR_INVALID_ARG
+    assert call(kv, _layout(mrp=0)) == rp.RP_ERR_INVALID_ARG and "max_resp_pages" in rp.last_error()
+    assert call(_kv(head_dim=96), lay) == rp.RP_ERR_UNSUPPORTED
+    # An empty batch launches nothing and needs no pointers.
+    assert call(kv, _layout(num_seqs=0), q=None, k=None, v=None, wq=None, wk=None, qo=None) == rp.RP_OK

@@ -1,0 +1,210 @@
+"""GPU parity of the decode step's pre-attention side through the C ABI.
+
+q (and the optional k copy) is compared with the fp64 oracle's correctly
+rounded bf16 bits: every element within one bf16 ulp, and all but a tiny
+fraction bit-identical (the kernel also computes in fp64 and rounds once).
+The pool after the append is compared byte for byte (codes and scales) with
+the append oracle applied to the kernel's own rotated k, so a rare one-ulp k
+difference cannot hide a wrong slot, page or scale decision. End-to-end
+cases run the whole decode step (prep, then attention over the advanced
+lengths) at the frontier operating point of 2 groups x 8 samples and compare
+it with the oracle's attention at the usual tolerances.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from tests.gpu_util import compare
+from workloads import make_qkprep_inputs, make_workload
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(msg):
+    print(f"[case] {msg}", flush=True)
+    sys.stdout.flush()
+
+
+def _bits(t):
+    return t.view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def _ulps(a, b):
+    """Distance in bf16 ulps between two bit arrays (signed zeros are equal)."""
+    def ordered(x):
+        m = (x & 0x7FFF).astype(np.int64)
+        return np.where(x & 0x8000, -m, m)
+    return np.abs(ordered(a) - ordered(b))
+
+
+def _check_bits(got, ref, label):
+    d = _ulps(got, ref)
+    exact = float((d == 0).mean()) if d.size else 1.0
+    assert d.max(initial=0) <= 1, f"{label}: max ulp distance {d.max()}"
+    assert exact >= 0.9999, f"{label}: only {exact:.6f} bit-identical"
+
+
+def _pool_bytes(b, kv_dtype):
+    view = (lambda t: _bits(t)) if kv_dtype == "bf16" else (lambda t: t.cpu().numpy())
+    out = [view(b.k_pages), view(b.v_pages)]
+    if kv_dtype == "fp8":
+        out += [b.k_scale.cpu().numpy(), b.v_scale.cpu().numpy()]
+    return out
+
+
+def _setup(S_groups, prefix_lens, resp_lens, Hq, Hkv, d, kv_dtype, seed, proj_scale=1.0, k_mult=1.0):
+    import paper_2606_26997_amd as rp
+    wl = make_workload(num_q_heads=Hq, num_kv_heads=Hkv, head_dim=d, seq_to_group=S_groups,
+                       prefix_lens=prefix_lens, resp_lens=resp_lens, seed=seed, append=True, kv_dtype=kv_dtype,
+                       k_mult=k_mult)
+    x = make_qkprep_inputs(num_seqs=wl.num_seqs, num_q_heads=Hq, num_kv_heads=Hkv, head_dim=d, seed=seed + 1,
+                           scale=proj_scale)
+    b = rp.DeviceBatch.from_workload(wl)
+    return wl, x, b
+
+
+def _oracle_prep(wl, x, resp_lens=None):
+    rl = wl.resp_lens if resp_lens is None else resp_lens
+    pos = oracle.decode_positions(wl.seq_to_group, wl.prefix_lens, rl)
+    qb, kb, _, _ = oracle.qk_prep(q_in=x.q_in, k_in=x.k_in, q_norm_w=x.q_norm_w, k_norm_w=x.k_norm_w, positions=pos)
+    return qb, kb
+
+
+def _oracle_pool(wl, x, k_bits, seqs=None):
+    """Append oracle on the kernel's rotated k (only for sequences ``seqs``, default all)."""
+    idx = np.arange(wl.num_seqs) if seqs is None else np.asarray(seqs)
+    return oracle.kv_append(k_pages=wl.k_pages, v_pages=wl.v_pages, k_scale=wl.k_scale, v_scale=wl.v_scale,
+                            kv_dtype=wl.kv_dtype, page_size=16, resp_lens=wl.resp_lens[idx],
+                            resp_block_table=wl.resp_block_table[idx], k_new=k_bits[idx], v_new=x.v_in[idx])
+
+
+CASES = [
+    # name, seq_to_group, prefix_lens, resp_lens, Hq, Hkv, d, kv dtype, projection scale, k_mult
+    ("ragged-d128", [0, 0, 1, 1, 1, 2, 2], [0, 17, 1000], [0, 15, 16, 31, 1, 47, 300], 16, 8, 128, "bf16", 1.0, 1.0),
+    ("ragged-d64", [0, 1, 1, 0], [33, 2], [5, 0, 64, 9], 4, 2, 64, "bf16", 1.0, 1.0),
+    ("mha-d64", [0, 0, 0], [12], [3, 16, 17], 4, 4, 64, "bf16", 1.0, 1.0),
+    ("fp8-requant", [0, 0, 1, 1, 1], [20, 40], [0, 5, 15, 16, 33], 16, 8, 128, "fp8", 4.0, 0.25),
+    ("fp8-keep", [0, 0, 1, 1], [20, 40], [3, 7, 9, 30], 16, 8, 128, "fp8", 0.25, 4.0),
+    ("fp8-d64", [0, 1, 0, 1], [8, 100], [1, 2, 17, 63], 8, 2, 64, "fp8", 2.0, 0.5),
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
+def test_qk_prep_and_append(case):
+    name, s2g, P, R, Hq, Hkv, d, dt, sc, km = case
+    _say(f"qk prep {name}")
+    wl, x, b = _setup(s2g, P, R, Hq, Hkv, d, dt, seed=len(name) * 7, proj_scale=sc, k_mult=km)
+    b.set_projections(x.q_in, x.k_in, x.v_in, x.q_norm_w, x.k_norm_w, keep_k=True)
+    b.qk_prep()
+    torch.cuda.synchronize()
+    qb, kb = _oracle_prep(wl, x)
+    _check_bits(_bits(b.q), qb, f"{name} q")
+    k_gpu = _bits(b.k_out)
+    _check_bits(k_gpu, kb, f"{name} k")
+    ref = _oracle_pool(wl, x, k_gpu)
+    got = _pool_bytes(b, dt)
+    for g, r, what in zip(got, ref, ("k pages", "v pages", "k scales", "v scales")):
+        np.testing.assert_array_equal(g, r, err_msg=f"{name}: {what}")
+    if dt == "fp8":
+        # The case exercises the scale branch it is named for on rows r > 0.
+        raised = []
+        for s in range(wl.num_seqs):
+            t = int(wl.resp_lens[s])
+            if t % 16:
+                page = int(wl.resp_block_table[s][t // 16])
+                raised += list(got[2][page] > wl.k_scale[page]) + list(got[3][page] > wl.v_scale[page])
+        assert raised and (any(raised) if name != "fp8-keep" else not any(raised)), name
+    # Same call again: the append is idempotent and q is recomputed identically.
+    q1 = _bits(b.q).copy()
+    b.qk_prep()
+    torch.cuda.synchronize()
+    assert np.array_equal(_bits(b.q), q1)
+    for g, r in zip(_pool_bytes(b, dt), ref):
+        assert np.array_equal(g, r), name
+
+
+def test_qk_prep_in_place_and_without_k_copy():
+    import paper_2606_26997_amd as rp
+    _say("qk prep in place")
+    wl, x, b = _setup([0, 0, 1], [64, 5], [2, 17, 33], 16, 8, 128, "bf16", seed=21)
+    b.set_projections(x.q_in, x.k_in, x.v_in, x.q_norm_w, x.k_norm_w, keep_k=False)
+    q = b.q_in  # q_out aliases q_in
+    rp.decode_qk_prep(b.kv, b.append_layout, q, b.k_in, b.v_in, b.q_norm_w, b.k_norm_w, q, None)
+    torch.cuda.synchronize()
+    qb, kb = _oracle_prep(wl, x)
+    _check_bits(_bits(q), qb, "in-place q")
+    # Without k_out the rotated k is only visible in the pool (bf16: the slot rows).
+    kp = _bits(b.k_pages)
+    for s in range(wl.num_seqs):
+        t = int(wl.resp_lens[s])
+        page = int(wl.resp_block_table[s][t // 16])
+        _check_bits(kp[page, :, t % 16], kb[s], f"pool k row of sequence {s}")
+
+
+def test_qk_prep_slot_outside_table_gets_q_but_no_append():
+    _say("qk prep slot outside the table")
+    wl, x, b = _setup([0, 0, 0], [16], [4, 20, 31], 8, 2, 64, "bf16", seed=5)
+    mrp = wl.resp_block_table.shape[1]
+    rl = wl.resp_lens.copy()
+    rl[1] = mrp * 16                      # one past the table: no slot
+    b.resp_lens.copy_(torch.from_numpy(rl))
+    b.set_projections(x.q_in, x.k_in, x.v_in, x.q_norm_w, x.k_norm_w, keep_k=True)
+    b.qk_prep()
+    torch.cuda.synchronize()
+    qb, kb = _oracle_prep(wl, x, resp_lens=rl)
+    _check_bits(_bits(b.q), qb, "q")
+    _check_bits(_bits(b.k_out), kb, "k")
+    ref = _oracle_pool(wl, x, _bits(b.k_out), seqs=[0, 2])
+    for g, r in zip(_pool_bytes(b, "bf16"), ref):
+        np.testing.assert_array_equal(g, r)
+
+
+@pytest.mark.parametrize("kv_dtype", ["bf16", "fp8"])
+def test_qk_prep_large_batch_one_block_per_sequence(kv_dtype):
+    # From 1024 sequences on, one block covers all heads of a sequence.
+    _say(f"qk prep 1100 sequences {kv_dtype}")
+    rng = np.random.default_rng(99)
+    S, G = 1100, 140
+    s2g = rng.integers(0, G, S)
+    wl, x, b = _setup(s2g, rng.integers(0, 64, G), rng.integers(0, 40, S), 16, 8, 128, kv_dtype, seed=31)
+    b.set_projections(x.q_in, x.k_in, x.v_in, x.q_norm_w, x.k_norm_w, keep_k=True)
+    b.qk_prep()
+    torch.cuda.synchronize()
+    qb, kb = _oracle_prep(wl, x)
+    _check_bits(_bits(b.q), qb, "q")
+    k_gpu = _bits(b.k_out)
+    _check_bits(k_gpu, kb, "k")
+    for g, r in zip(_pool_bytes(b, kv_dtype), _oracle_pool(wl, x, k_gpu)):
+        np.testing.assert_array_equal(g, r)
+
+
+@pytest.mark.parametrize("kv_dtype", ["bf16", "fp8"])
+def test_decode_step_at_frontier_operating_point(kv_dtype):
+    # Two groups of eight live samples (the frontier batch of 16 sequences):
+    # 1k-token prompts, ragged responses up to ~3.5k tokens.
+    _say(f"decode step 2x8 {kv_dtype}")
+    rng = np.random.default_rng(7)
+    s2g = np.repeat([0, 1], 8)
+    R = rng.integers(1, 3500, 16)
+    wl, x, b = _setup(s2g, [1024, 977], R, 16, 8, 128, kv_dtype, seed=41)
+    b.set_projections(x.q_in, x.k_in, x.v_in, x.q_norm_w, x.k_norm_w)
+    b.decode_step()
+    torch.cuda.synchronize()
+    qb, kb, pool = oracle.decode_step_prep(q_in=x.q_in, k_in=x.k_in, v_in=x.v_in, q_norm_w=x.q_norm_w,
+                                           k_norm_w=x.k_norm_w, k_pages=wl.k_pages, v_pages=wl.v_pages,
+                                           k_scale=wl.k_scale, v_scale=wl.v_scale, kv_dtype=kv_dtype,
+                                           page_size=16, seq_to_group=wl.seq_to_group, prefix_lens=wl.prefix_lens,
+                                           resp_lens=wl.resp_lens, resp_block_table=wl.resp_block_table)
+    _check_bits(_bits(b.q), qb, "q")
+    kp, vp, ks, vs = pool
+    ref_out, ref_lse = oracle.decode_attention(k_pages=kp, v_pages=vp, k_scale=ks, v_scale=vs, kv_dtype=kv_dtype,
+                                               page_size=16, seq_to_group=wl.seq_to_group,
+                                               prefix_lens=wl.prefix_lens, prefix_block_table=wl.prefix_block_table,
+                                               resp_lens=wl.resp_lens + 1, resp_block_table=wl.resp_block_table,
+                                               q=qb, softmax_scale=wl.softmax_scale)
+    out = b.out.float().cpu().numpy().astype(np.float64)
+    lse = b.lse.cpu().numpy().astype(np.float64)
+    compare(out, lse, ref_out, ref_lse, kv_dtype, label=f"decode step {kv_dtype}")
