@@ -51,6 +51,9 @@ def parse_args():
                         "attention) on the workload's prompts instead of the decode step")
     p.add_argument("--prefill-len", type=int, default=None,
                    help="with --prefill: every prompt this many tokens instead of the workload's lengths")
+    p.add_argument("--fgd", action="store_true",
+                   help="time the whole decode step (q/k norm + rotary + append, plan, attention, combine) at "
+                        "the frontier operating point: 2 groups x 8 live samples")
     p.add_argument("--traffic-from", metavar="DIR", default=None,
                    help="summarise rocprofv3 --pmc runs under DIR (pmc_fetch, pmc_write, pmc_copy_fetch, "
                         "pmc_copy_write) into the stored HBM traffic of the partial-attention kernel")
@@ -249,6 +252,106 @@ def prefill_bench(args):
     print(json.dumps(line), flush=True)
 
 
+FGD_GROUPS, FGD_LIVE, FGD_PREFIX, FGD_RESP_MAX = 2, 8, 512, 6016
+
+
+def fgd_bench(args):
+    """One decode step of one layer at the frontier operating point.
+
+    Frontier-group dispatch keeps F_w = 2 groups of K = 8 samples in flight, so
+    the live batch is 16 sequences. Each group has a 512-token prompt; the
+    responses are uniform in [0, 6016], about 3.5k tokens of context per
+    sequence on average. Qwen3-1.7B layer shape, bf16 KV. A step starts from
+    the raw projections: q/k RMS norm and rotary embedding with the k/v append,
+    then the plan, the partial results and the combine.
+    """
+    import numpy as np
+    import torch
+    import paper_2606_26997_amd as rp
+    from workloads import make_qkprep_inputs, make_workload
+
+    seed = 2026 if args.seed is None else args.seed
+    rng = np.random.default_rng(seed)
+    S = FGD_GROUPS * FGD_LIVE
+    resp = rng.integers(0, FGD_RESP_MAX + 1, S)
+    wl = make_workload(num_q_heads=16, num_kv_heads=8, head_dim=128, seq_to_group=np.repeat(np.arange(FGD_GROUPS), FGD_LIVE),
+                       prefix_lens=np.full(FGD_GROUPS, FGD_PREFIX), resp_lens=resp, seed=seed, append=True,
+                       k_mult=0.5, rng=rng)
+    x = make_qkprep_inputs(num_seqs=S, num_q_heads=16, num_kv_heads=8, head_dim=128, seed=seed + 1)
+    torch.cuda.set_device(0)
+    b = rp.DeviceBatch.from_workload(wl, device="cuda:0")
+    b.set_projections(x.q_in, x.k_in, x.v_in, x.q_norm_w, x.k_norm_w)
+    bm = byte_model(wl)
+    prep_extra = 2 * S * wl.num_q_heads * wl.head_dim * 2      # raw q read and prepared q written
+    total = bm["total"] + prep_extra
+    stages = ["prep", "plan", "parts", "combine"]
+    calls = {"prep": b.qk_prep, "plan": b.plan, "parts": b.attn_parts, "combine": b.combine_parts}
+
+    def step(evs=None):
+        for i, name in enumerate(stages):
+            if evs is not None:
+                evs[i].record()
+            calls[name]()
+        if evs is not None:
+            evs[len(stages)].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) / args.steps * 1e3
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(len(stages) + 1)] for _ in range(args.steps)]
+    for k in range(args.steps):
+        step(events[k])
+    torch.cuda.synchronize()
+    per = {name: float(np.mean([events[k][i].elapsed_time(events[k][i + 1]) for k in range(args.steps)])) * 1e3
+           for i, name in enumerate(stages)}
+    parts_us = per["parts"]
+    achieved = bm["parts_kernel"] / (parts_us * 1e-6) / 1e9
+
+    # The prep kernel alone on a large batch (4096 sequences, one response page
+    # each): q read and written, k and v read and appended.
+    S2 = 4096
+    wl2 = make_workload(num_q_heads=16, num_kv_heads=8, head_dim=128, seq_to_group=np.arange(S2) // 8,
+                        prefix_lens=np.full(S2 // 8, 16), resp_lens=rng.integers(0, 15, S2), seed=seed + 2,
+                        append=True, rng=rng)
+    x2 = make_qkprep_inputs(num_seqs=S2, num_q_heads=16, num_kv_heads=8, head_dim=128, seed=seed + 3)
+    b2 = rp.DeviceBatch.from_workload(wl2, device="cuda:0")
+    b2.set_projections(x2.q_in, x2.k_in, x2.v_in, x2.q_norm_w, x2.k_norm_w)
+    for _ in range(args.warmup):
+        b2.qk_prep()
+    ev2 = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    for a, c in ev2:
+        a.record()
+        b2.qk_prep()
+        c.record()
+    torch.cuda.synchronize()
+    prep_us = float(np.mean([a.elapsed_time(c) for a, c in ev2])) * 1e3
+    prep_bytes = S2 * (2 * 16 + 4 * 8) * 128 * 2
+    line = {
+        "metric": "decode step at the frontier operating point: seq-steps/s per layer and achieved HBM GB/s",
+        "value": round(S / (ms * 1e-3), 1), "unit": "seq-steps/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"frontier batch: {FGD_GROUPS} groups x {FGD_LIVE} live samples, prompt "
+                               f"{FGD_PREFIX}, responses uniform [0, {FGD_RESP_MAX}]",
+                   "seqs": S, "q_heads": 16, "kv_heads": 8, "head_dim": 128, "kv_dtype": "bf16",
+                   "prefix_tokens": bm["prefix_tokens"], "resp_tokens": bm["resp_tokens"], "seed": seed},
+        "GBps": round(total / (ms * 1e-3) / 1e9, 1), "algorithmic_bytes_per_step": int(total),
+        "kernel_us": {k: round(v, 2) for k, v in per.items()},
+        "prep_4096_seqs": {"us": round(prep_us, 2), "bytes": prep_bytes,
+                           "GBps": round(prep_bytes / (prep_us * 1e-6) / 1e9, 1)},
+        "roofline": {"kernel": "attn_parts_kernel", "bound": "hbm", "achieved": round(achieved, 1),
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                     "traffic": None, "algorithmic_bytes_per_launch": int(bm["parts_kernel"])},
+        "cpu_baseline": None,
+    }
+    print(json.dumps(line), flush=True)
+
+
 def main():
     args = parse_args()
     if args.gpus != 1:
@@ -267,6 +370,9 @@ def main():
         return
     if args.prefill:
         prefill_bench(args)
+        return
+    if args.fgd:
+        fgd_bench(args)
         return
 
     import paper_2606_26997_amd as rp

@@ -133,15 +133,17 @@ rp_status rp_kv_append(const rp_paged_kv* kv, const rp_group_layout* layout,
  * Computed in fp64 from the bf16 inputs and rounded once to bf16 (nearest
  * even): outputs equal the correctly rounded values except where the exact
  * value lies within a few fp64 ulps of a rounding boundary (then they are
- * one bf16 ulp away).
+ * one bf16 ulp away). The rotary frequencies theta^(-2i/d) are computed on
+ * the host with the C library's pow.
  * q_in: bf16 [S][Hq][d]; k_in, v_in: bf16 [S][Hkv][d]; q_norm_w, k_norm_w:
- * bf16 [d]; q_out: bf16 [S][Hq][d] (the q layout rp_group_decode_attn reads),
- * may be q_in itself but must not otherwise overlap it; k_out: bf16
- * [S][Hkv][d] copy of the rotated k, or NULL. The rotated k and the
- * unchanged v are appended exactly as rp_kv_append would append them (same
- * slot, same fp8 rule); a sequence with resp_lens[s] outside
- * [0, max_resp_pages * 16) gets q_out (and k_out) but no append. rms_eps must
- * be finite and >= 0 (Qwen3: 1e-6), rope_theta finite and > 0 (Qwen3: 1e6). */
+ * bf16 [d]; q_out: bf16 [S][Hq][d] (the q layout rp_group_decode_attn reads);
+ * all 16-byte aligned. q_out may be q_in itself but must not otherwise
+ * overlap it. k_out: bf16 [S][Hkv][d] copy of the rotated k, or NULL. The
+ * rotated k and the unchanged v are appended exactly as rp_kv_append would
+ * append them (same slot, same fp8 rule); a sequence with resp_lens[s]
+ * outside [0, max_resp_pages * 16) gets q_out (and k_out) but no append.
+ * rms_eps must be finite and >= 0 (Qwen3: 1e-6; with 0, an all-zero head
+ * gives NaN), rope_theta finite and > 0 (Qwen3: 1e6). */
 rp_status rp_decode_qk_prep(const rp_paged_kv* kv, const rp_group_layout* layout,
                             const void* q_in, const void* k_in, const void* v_in,
                             const void* q_norm_w, const void* k_norm_w,

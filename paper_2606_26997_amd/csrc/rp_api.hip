@@ -359,9 +359,9 @@ rp_status rp_decode_qk_prep(const rp_paged_kv* kv, const rp_group_layout* l, con
   if (sh.S == 0) return RP_OK;
   const void* in[] = {q_in, k_in, v_in, q_norm_w, k_norm_w, q_out};
   for (const void* p : in)
-    if (p == nullptr || !aligned(p, 2))
-      return fail(RP_ERR_INVALID_ARG, "q_in/k_in/v_in/q_norm_w/k_norm_w/q_out must be non-NULL bf16 arrays");
-  if (k_out != nullptr && !aligned(k_out, 2)) return fail(RP_ERR_INVALID_ARG, "k_out must be a bf16 array");
+    if (p == nullptr || !aligned(p, 16))
+      return fail(RP_ERR_INVALID_ARG, "q_in/k_in/v_in/q_norm_w/k_norm_w/q_out must be non-NULL and 16-byte aligned");
+  if (k_out != nullptr && !aligned(k_out, 16)) return fail(RP_ERR_INVALID_ARG, "k_out must be 16-byte aligned");
   if (sh.max_rp < 1) return fail(RP_ERR_INVALID_ARG, "max_resp_pages must be >= 1 to append");
   rp::QkPrepArgs a;
   a.k_pages = kv->k_pages;
@@ -384,10 +384,12 @@ rp_status rp_decode_qk_prep(const rp_paged_kv* kv, const rp_group_layout* l, con
   a.q_norm_w = static_cast<const uint16_t*>(q_norm_w);
   a.k_norm_w = static_cast<const uint16_t*>(k_norm_w);
   a.rms_eps = rms_eps;
-  a.rope_theta = rope_theta;
+  // Rotary frequencies on the host in fp64 (libm pow), passed with the arguments.
+  for (int i = 0; i < rp::kMaxHeadDim / 2; ++i)
+    a.inv_freq[i] = i < sh.D / 2 ? std::pow(rope_theta, (-2.0 * i) / sh.D) : 0.0;
   a.q_out = static_cast<uint16_t*>(q_out);
   a.k_out = static_cast<uint16_t*>(k_out);
-  a.blocks_per_seq = a.heads_per_block = 0;
+  a.blocks_per_seq = 0;
   hipError_t e = rp::launch_qk_prep(a, sh.D, sh.fp8, stream);
   return e == hipSuccess ? RP_OK : hip_fail(e, "decode q/k prep kernel launch");
 }

@@ -41,8 +41,9 @@ __global__ __launch_bounds__(64) void append_kernel(const AppendArgs a) {
       kx[e] = __uint_as_float((uint32_t)kn[64 * e + lane] << 16);
       vx[e] = __uint_as_float((uint32_t)vn[64 * e + lane] << 16);
     }
-    append_fp8_row<D>(static_cast<uint8_t*>(a.k_pages) + blk, a.k_scale + sidx, r, kx, lane);
-    append_fp8_row<D>(static_cast<uint8_t*>(a.v_pages) + blk, a.v_scale + sidx, r, vx, lane);
+    const auto col = [lane](int e) { return lane + 64 * e; };
+    append_fp8_row<D, 64>(static_cast<uint8_t*>(a.k_pages) + blk, a.k_scale + sidx, r, kx, col, lane == 0);
+    append_fp8_row<D, 64>(static_cast<uint8_t*>(a.v_pages) + blk, a.v_scale + sidx, r, vx, col, lane == 0);
   }
 }
 

@@ -115,22 +115,24 @@ __device__ inline uint32_t f32_to_e4m3(float x) {
 }
 
 // ---- the fp8 append rule --------------------------------------------------
-// Row r of an fp8 (page, kv-head) block [16][D] takes a new token x; lane
-// `lane` holds columns lane + 64 e of it (fp32 values of bf16 inputs).
-// amax = max |x| over the row; row 0 sets scale = amax / 448 (1 when amax is
-// 0); a later row keeps the old scale when amax <= 448 * old, and otherwise
-// sets scale = amax / 448 after requantising rows 0..r-1 from code * old.
-// Plain IEEE fp32 (no contraction, correctly rounded division), so the bytes
-// are a deterministic function of the inputs. The whole wave must call it.
-template <int D>
-__device__ void append_fp8_row(uint8_t* blk, float* scale_slot, int r, const float (&x)[D / 64], int lane) {
+// Row r of an fp8 (page, kv-head) block [16][D] takes a new token x. An
+// aligned group of G lanes holds the row: element e of a lane sits at column
+// col(e) (fp32 values of bf16 inputs); `leader` marks the one lane that
+// stores the scale. amax = max |x| over the row; row 0 sets
+// scale = amax / 448 (1 when amax is 0); a later row keeps the old scale when
+// amax <= 448 * old, and otherwise sets scale = amax / 448 after requantising
+// rows 0..r-1 from code * old. Plain IEEE fp32 (no contraction, correctly
+// rounded division), so the bytes are a deterministic function of the inputs.
+// Every lane of the wave must call it with the same r.
+template <int D, int G, int N, class ColFn>
+__device__ void append_fp8_row(uint8_t* blk, float* scale_slot, int r, const float (&x)[N], ColFn col,
+                               bool leader) {
 #pragma clang fp contract(off)
-  constexpr int EPL = D / 64;
   float amax = 0.f;
 #pragma unroll
-  for (int e = 0; e < EPL; ++e) amax = fmaxf(amax, fabsf(x[e]));
+  for (int e = 0; e < N; ++e) amax = fmaxf(amax, fabsf(x[e]));
 #pragma unroll
-  for (int o = 1; o < 64; o <<= 1) amax = fmaxf(amax, __shfl_xor(amax, o));
+  for (int o = 1; o < G; o <<= 1) amax = fmaxf(amax, __shfl_xor(amax, o));
   const float old = *scale_slot;
   float scale;
   if (r == 0) {
@@ -140,18 +142,18 @@ __device__ void append_fp8_row(uint8_t* blk, float* scale_slot, int r, const flo
   } else {
     scale = amax / 448.0f;
     for (int rr = 0; rr < r; ++rr) {
-      uint8_t* row = blk + (size_t)rr * D + lane;
+      uint8_t* row = blk + (size_t)rr * D;
 #pragma unroll
-      for (int e = 0; e < EPL; ++e) {
-        const float val = e4m3_to_f32(row[64 * e]) * old;
-        row[64 * e] = (uint8_t)f32_to_e4m3(val / scale);
+      for (int e = 0; e < N; ++e) {
+        const float val = e4m3_to_f32(row[col(e)]) * old;
+        row[col(e)] = (uint8_t)f32_to_e4m3(val / scale);
       }
     }
   }
-  uint8_t* row = blk + (size_t)r * D + lane;
+  uint8_t* row = blk + (size_t)r * D;
 #pragma unroll
-  for (int e = 0; e < EPL; ++e) row[64 * e] = (uint8_t)f32_to_e4m3(x[e] / scale);
-  if (lane == 0) *scale_slot = scale;
+  for (int e = 0; e < N; ++e) row[col(e)] = (uint8_t)f32_to_e4m3(x[e] / scale);
+  if (leader) *scale_slot = scale;
 }
 
 // ---- wavefront reductions -----------------------------------------------

@@ -78,6 +78,8 @@ struct AppendArgs {
   const void* v_new;
 };
 
+constexpr int kMaxHeadDim = 128;
+
 // Pre-attention side of a decode step: q/k RMS norm + rotary embedding,
 // q written out, k and v appended at response slot resp_lens[s].
 struct QkPrepArgs {
@@ -96,10 +98,11 @@ struct QkPrepArgs {
   const uint16_t* v_in;
   const uint16_t* q_norm_w;  // bf16 [D]
   const uint16_t* k_norm_w;
-  double rms_eps, rope_theta;
+  double rms_eps;
+  double inv_freq[kMaxHeadDim / 2];  // rotary frequency of pair i: theta^(-2i/D)
   uint16_t* q_out;           // bf16 [S][Hq][D]
   uint16_t* k_out;           // bf16 [S][Hkv][D] or null
-  int blocks_per_seq, heads_per_block;  // set by the launcher
+  int blocks_per_seq;        // set by the launcher
 };
 
 // Shared-prefix prefill: packed prompt tokens of every group (group g owns

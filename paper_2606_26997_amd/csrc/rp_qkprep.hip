@@ -2,169 +2,246 @@
 // For sequence s (group g = seq_to_group[s]) the new token sits at position
 // prefix_lens[g] + resp_lens[s]. Every q head and k head is RMS-normalised
 // with the layer's per-channel weights and rotated by the rotary embedding
-// (pairs (i, i + D/2), angle position * theta^(-2i/D)); q goes to q_out, k
-// and the unchanged v are appended at response slot resp_lens[s] (bf16 copy
-// or the fp8 append rule).
+// (pairs (i, i + D/2), angle position * inv_freq[i]); q goes to q_out, k and
+// the unchanged v are appended at response slot resp_lens[s] (bf16 copy or
+// the fp8 append rule).
 //
 // The arithmetic is fp64 on the bf16 inputs with one rounding to bf16 at the
 // end, so each output is the correctly rounded value unless the exact value
-// lies within a few fp64 ulps of a bf16 rounding boundary. The angles are
-// computed once per block into LDS.
+// lies within a few fp64 ulps of a bf16 rounding boundary.
 //
-// Grid: blocks of 4 waves; one block covers heads_per_block of the Hq + Hkv
-// heads of one sequence, wave w taking heads h0 + w, h0 + w + 4, ...; q head
-// j < Hq, kv-head j - Hq otherwise. Lane l handles columns l + 64 e.
+// Work split: a sequence has Hq + 2 Hkv head slots (q heads, k heads, v
+// heads); a group of 16 lanes owns one slot (or two, j and j + 16, on large
+// batches), a block of 256 threads 16 (32) slots of one sequence, all of
+// their loads in flight at once. Lane l of a group holds the D/32 pairs l*D/32 + p, that is
+// columns l*D/32 + p and D/2 + l*D/32 + p, so each pair is rotated in-lane and
+// every row is read and written as whole 16-lane runs. Each block computes
+// the cos/sin of the D/2 angles of its sequence once, folded with the norm
+// weights into LDS tables.
 #include "rp_device.h"
 #include "rp_internal.h"
 
 namespace rp {
 namespace {
 
-constexpr int kPrepWaves = 4;
-constexpr int kPrepThreads = 64 * kPrepWaves;
+constexpr int kSlotLanes = 16;
+constexpr int kPrepThreads = 256;
+constexpr int kGroups = kPrepThreads / kSlotLanes;
 
-// fp64 -> bf16 bits with a single rounding to nearest even. Below 2^-126 the
-// bf16 grid is the subnormal step 2^-133; above, the 52-bit mantissa is
-// rounded to 7 bits on the integer pattern (a carry bumps the exponent) and
-// the result converts to fp32 exactly. Finite inputs (NaN maps to 0x7FC0).
-__device__ inline uint32_t f64_to_bf16_rne(double x) {
-  const unsigned long long u = (unsigned long long)__double_as_longlong(x);
-  const uint32_t sign = (uint32_t)(u >> 48) & 0x8000u;
-  const unsigned long long a = u & 0x7FFFFFFFFFFFFFFFull;
-  if (a > 0x7FF0000000000000ull) return 0x7FC0u;
-  if (a < 0x3810000000000000ull) {                     // |x| < 2^-126
-    const double q = rint(__longlong_as_double((long long)a) * 0x1p133);  // exact scaling
-    return sign | (uint32_t)q;                          // 0..128; 128 is 2^-126
-  }
-  const unsigned long long r = (a + 0x00000FFFFFFFFFFFull + ((a >> 45) & 1ull)) & ~0x00001FFFFFFFFFFFull;
-  const float f = (float)__longlong_as_double((long long)r);  // exact (inf past the bf16 range)
-  return sign | (__float_as_uint(f) >> 16);
+// fp64 -> bf16 bits, one rounding to nearest even, in two steps: the fp32
+// rounding f of y, then f's own rounding to bf16 (gfx950's packed
+// conversion, nearest even). That is the single rounding of y except when f
+// lands exactly on a bf16 tie while y does not; then y's side of the tie
+// decides (bf16_tie_fix). bf16_tie reports that case.
+__device__ inline uint32_t pack_bf16_rne(float lo, float hi) {
+  typedef __bf16 bf16x2_v __attribute__((ext_vector_type(2)));
+  typedef float f32x2_v __attribute__((ext_vector_type(2)));
+  const f32x2_v v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_v));
+}
+__device__ inline bool bf16_tie(float f) { return (__float_as_uint(f) & 0xFFFFu) == 0x8000u; }
+__device__ inline uint32_t bf16_tie_fix(double y, float f) {
+  const uint32_t u = __float_as_uint(f);
+  const double d = y - (double)f;  // exact
+  if (d == 0.0) return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+  return (u >> 16) + ((d > 0.0) == ((u >> 31) == 0u) ? 1u : 0u);
+}
+__device__ inline void set_half(uint32_t& w, int hi, uint32_t v) {
+  w = hi ? (w & 0xFFFFu) | (v << 16) : (w & 0xFFFF0000u) | v;
 }
 
-__device__ inline double wave_sum_f64(double v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
-  return v;
-}
-
-// RMS norm and rotary embedding of one head (all lanes of the wave), rounded
-// to bf16 bits.
-template <int D>
-__device__ inline void norm_rope(const uint16_t* src, const uint16_t* w, double eps, const double* s_cos,
-                                 const double* s_sin, int lane, uint32_t (&out)[D / 64]) {
-  constexpr int EPL = D / 64;
-  double x[EPL];
-  double ss = 0.0;
-#pragma unroll
-  for (int e = 0; e < EPL; ++e) {
-    x[e] = (double)__uint_as_float((uint32_t)src[64 * e + lane] << 16);
-    ss += x[e] * x[e];
-  }
-  const double den = sqrt(wave_sum_f64(ss) / D + eps);
-#pragma unroll
-  for (int e = 0; e < EPL; ++e) x[e] = x[e] / den * (double)__uint_as_float((uint32_t)w[64 * e + lane] << 16);
-  if constexpr (EPL == 2) {
-    // Columns lane and lane + 64 form pair `lane`.
-    const double c = s_cos[lane], sn = s_sin[lane];
-    out[0] = f64_to_bf16_rne(x[0] * c - x[1] * sn);
-    out[1] = f64_to_bf16_rne(x[1] * c + x[0] * sn);
+// W 32-bit words (2W bf16) starting at element `col` of a row.
+template <int W>
+__device__ inline void load_words(const uint16_t* row, int col, uint32_t (&w)[W]) {
+  if constexpr (W == 2) {
+    const uint2 v = *reinterpret_cast<const uint2*>(row + col);
+    w[0] = v.x;
+    w[1] = v.y;
   } else {
-    // Column lane pairs with lane ^ 32.
-    const double p = __shfl_xor(x[0], 32);
-    const double c = s_cos[lane & 31], sn = s_sin[lane & 31];
-    out[0] = f64_to_bf16_rne(lane < 32 ? x[0] * c - p * sn : x[0] * c + p * sn);
+    w[0] = *reinterpret_cast<const uint32_t*>(row + col);
   }
+}
+template <int W>
+__device__ inline void store_words(uint16_t* row, int col, const uint32_t (&w)[W]) {
+  if constexpr (W == 2) {
+    *reinterpret_cast<uint2*>(row + col) = make_uint2(w[0], w[1]);
+  } else {
+    *reinterpret_cast<uint32_t*>(row + col) = w[0];
+  }
+}
+
+__device__ inline double bf16_word_f64(const uint32_t* w, int p) {
+  return (double)(p & 1 ? bf16_hi(w[p >> 1]) : bf16_lo(w[p >> 1]));
 }
 
 template <int D, bool FP8>
-__global__ __launch_bounds__(kPrepThreads) void qk_prep_kernel(const QkPrepArgs a) {
-  constexpr int EPL = D / 64;
+__device__ inline void prep_slot(const QkPrepArgs& a, int s, int kind, int head, int l16, int L,
+                                 const uint32_t (&x1)[D / 64], const uint32_t (&x2)[D / 64],
+                                 const double (*s_tab)[4][D / 2]) {
+  constexpr int NP = D / 32;   // pairs per lane
+  constexpr int W = NP / 2;    // 32-bit words per lane and half row
   constexpr int HALF = D / 2;
-  __shared__ double s_cos[HALF], s_sin[HALF];
   const int Hq = a.num_q_heads, Hkv = a.num_kv_heads;
-  const int s = blockIdx.x / a.blocks_per_seq;
-  const int h0 = (blockIdx.x - s * a.blocks_per_seq) * a.heads_per_block;
-  const int h1 = min(h0 + a.heads_per_block, Hq + Hkv);
-  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-  const int g = clamp_group(a.seq_to_group[s], a.num_groups);
-  const int L = a.resp_lens[s];
-  if (t < HALF) {
-    const double pos = (double)a.prefix_lens[g] + (double)L;
-    double sn, cs;
-    sincos(pos * pow(a.rope_theta, (-2.0 * t) / D), &sn, &cs);
-    s_cos[t] = cs;
-    s_sin[t] = sn;
-  }
-  __syncthreads();
-
-  const bool slot_ok = L >= 0 && L < a.max_resp_pages * kPage;
-  int page = 0;
-  if (slot_ok) page = clamp_page(a.resp_block_table[(size_t)s * a.max_resp_pages + L / kPage], a.num_pages);
-  const int r = L % kPage;
-
-  for (int j = h0 + wave; j < h1; j += kPrepWaves) {
-    uint32_t o[EPL];
-    if (j < Hq) {
-      const size_t off = ((size_t)s * Hq + j) * D;
-      norm_rope<D>(a.q_in + off, a.q_norm_w, a.rms_eps, s_cos, s_sin, lane, o);
+  const int c1 = l16 * NP, c2 = HALF + l16 * NP;  // first columns of the lane's two runs
+  uint32_t o1[W], o2[W];
+  if (kind == 2) {
 #pragma unroll
-      for (int e = 0; e < EPL; ++e) a.q_out[off + 64 * e + lane] = (uint16_t)o[e];
-      continue;
+    for (int k = 0; k < W; ++k) {
+      o1[k] = x1[k];
+      o2[k] = x2[k];
     }
-    const int h = j - Hq;
-    const size_t off = ((size_t)s * Hkv + h) * D;
-    norm_rope<D>(a.k_in + off, a.k_norm_w, a.rms_eps, s_cos, s_sin, lane, o);
-    uint32_t vb[EPL];
+  } else {
+    double y1[NP], y2[NP];
+    double ss = 0.0;
 #pragma unroll
-    for (int e = 0; e < EPL; ++e) vb[e] = a.v_in[off + 64 * e + lane];
+    for (int p = 0; p < NP; ++p) {
+      y1[p] = bf16_word_f64(x1, p);
+      y2[p] = bf16_word_f64(x2, p);
+      ss += y1[p] * y1[p] + y2[p] * y2[p];
+    }
+#pragma unroll
+    for (int o = kSlotLanes / 2; o >= 1; o >>= 1) ss += __shfl_xor(ss, o);
+    // 1 / sqrt(mean + eps): hardware estimate refined by two Newton steps
+    // (a few fp64 ulps).
+    const double m = ss / D + a.rms_eps;
+    const double hm = 0.5 * m;
+    double inv = __builtin_amdgcn_rsq(m);
+    inv = inv * fma(-hm * inv, inv, 1.5);
+    inv = inv * fma(-hm * inv, inv, 1.5);
+    const double(*tab)[HALF] = s_tab[kind];
+    double z1[NP], z2[NP];
+    float f1[NP], f2[NP];
+    bool tie = false;
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+      const int i = c1 + p;
+      z1[p] = inv * fma(y1[p], tab[0][i], -(y2[p] * tab[1][i]));
+      z2[p] = inv * fma(y2[p], tab[2][i], y1[p] * tab[3][i]);
+      f1[p] = (float)z1[p];
+      f2[p] = (float)z2[p];
+      tie = tie || bf16_tie(f1[p]) || bf16_tie(f2[p]);
+    }
+#pragma unroll
+    for (int k = 0; k < W; ++k) {
+      o1[k] = pack_bf16_rne(f1[2 * k], f1[2 * k + 1]);
+      o2[k] = pack_bf16_rne(f2[2 * k], f2[2 * k + 1]);
+    }
+    if (tie) {  // rare: some fp32 value sits exactly on a bf16 tie
+#pragma unroll
+      for (int p = 0; p < NP; ++p) {
+        if (bf16_tie(f1[p])) set_half(o1[p >> 1], p & 1, bf16_tie_fix(z1[p], f1[p]));
+        if (bf16_tie(f2[p])) set_half(o2[p >> 1], p & 1, bf16_tie_fix(z2[p], f2[p]));
+      }
+    }
+    if (kind == 0) {
+      uint16_t* dst = a.q_out + ((size_t)s * Hq + head) * D;
+      store_words<W>(dst, c1, o1);
+      store_words<W>(dst, c2, o2);
+      return;
+    }
     if (a.k_out != nullptr) {
-#pragma unroll
-      for (int e = 0; e < EPL; ++e) a.k_out[off + 64 * e + lane] = (uint16_t)o[e];
+      uint16_t* dst = a.k_out + ((size_t)s * Hkv + head) * D;
+      store_words<W>(dst, c1, o1);
+      store_words<W>(dst, c2, o2);
     }
-    if (!slot_ok) continue;
-    const size_t blk = ((size_t)page * Hkv + h) * kPage * D;  // in elements
-    if constexpr (!FP8) {
-      uint16_t* kd = static_cast<uint16_t*>(a.k_pages) + blk + (size_t)r * D + lane;
-      uint16_t* vd = static_cast<uint16_t*>(a.v_pages) + blk + (size_t)r * D + lane;
+  }
+
+  // Append of k (kind 1) or v (kind 2) at response slot L.
+  if (L < 0 || L >= a.max_resp_pages * kPage) return;  // no slot for the new token
+  const int page = clamp_page(a.resp_block_table[(size_t)s * a.max_resp_pages + L / kPage], a.num_pages);
+  const int r = L % kPage;
+  const size_t blk = ((size_t)page * Hkv + head) * kPage * D;  // in elements
+  if constexpr (!FP8) {
+    uint16_t* dst = static_cast<uint16_t*>(kind == 1 ? a.k_pages : a.v_pages) + blk + (size_t)r * D;
+    store_words<W>(dst, c1, o1);
+    store_words<W>(dst, c2, o2);
+  } else {
+    float xf[2 * NP];
 #pragma unroll
-      for (int e = 0; e < EPL; ++e) {
-        kd[64 * e] = (uint16_t)o[e];
-        vd[64 * e] = (uint16_t)vb[e];
-      }
-    } else {
-      const size_t sidx = (size_t)page * Hkv + h;
-      float kx[EPL], vx[EPL];
-#pragma unroll
-      for (int e = 0; e < EPL; ++e) {
-        kx[e] = __uint_as_float(o[e] << 16);
-        vx[e] = __uint_as_float(vb[e] << 16);
-      }
-      append_fp8_row<D>(static_cast<uint8_t*>(a.k_pages) + blk, a.k_scale + sidx, r, kx, lane);
-      append_fp8_row<D>(static_cast<uint8_t*>(a.v_pages) + blk, a.v_scale + sidx, r, vx, lane);
+    for (int p = 0; p < NP; ++p) {
+      xf[p] = p & 1 ? bf16_hi(o1[p >> 1]) : bf16_lo(o1[p >> 1]);
+      xf[NP + p] = p & 1 ? bf16_hi(o2[p >> 1]) : bf16_lo(o2[p >> 1]);
     }
+    const auto col = [c1, c2](int e) { return e < NP ? c1 + e : c2 + (e - NP); };
+    uint8_t* pages = static_cast<uint8_t*>(kind == 1 ? a.k_pages : a.v_pages);
+    float* scales = kind == 1 ? a.k_scale : a.v_scale;
+    append_fp8_row<D, kSlotLanes>(pages + blk, scales + (size_t)page * Hkv + head, r, xf, col, l16 == 0);
   }
 }
 
-template <int D>
-hipError_t launch_d(const QkPrepArgs& a, bool fp8, hipStream_t stream) {
+template <int D, bool FP8, int SPL>
+__global__ __launch_bounds__(kPrepThreads) void qk_prep_kernel(const QkPrepArgs a) {
+  constexpr int W = D / 64;
+  constexpr int HALF = D / 2;
+  // Per pair i and weight set (0: q, 1: k): A = w[i] cos, B = w[i + D/2] sin,
+  // C = w[i + D/2] cos, E = w[i] sin, so that with the norm factor inv
+  //   out[i] = inv (x[i] A - x[i + D/2] B),  out[i + D/2] = inv (x[i + D/2] C + x[i] E).
+  __shared__ double s_tab[2][4][HALF];
+  const int Hq = a.num_q_heads, Hkv = a.num_kv_heads;
+  const int t = threadIdx.x, l16 = t & (kSlotLanes - 1);
+  const int s = blockIdx.x / a.blocks_per_seq;
+  const int slot0 = (blockIdx.x - s * a.blocks_per_seq) * (kGroups * SPL) + t / kSlotLanes;
+  const int c1 = l16 * (D / 32), c2 = HALF + l16 * (D / 32);
+  const int g = clamp_group(a.seq_to_group[s], a.num_groups);
+  const int L = a.resp_lens[s];
+
+  // The lane's slots slot0 + 16 k (k < SPL); kind 0 = q head, 1 = k head,
+  // 2 = v head. Every load is issued before the tables are built.
+  int kind[SPL], head[SPL];
+  uint32_t x1[SPL][W], x2[SPL][W];
+#pragma unroll
+  for (int k = 0; k < SPL; ++k) {
+    const int slot = slot0 + k * kGroups;
+    kind[k] = slot < Hq ? 0 : (slot < Hq + Hkv ? 1 : (slot < Hq + 2 * Hkv ? 2 : 3));
+    head[k] = kind[k] == 0 ? slot : (kind[k] == 1 ? slot - Hq : slot - Hq - Hkv);
+    if (kind[k] < 3) {
+      const uint16_t* src = kind[k] == 0 ? a.q_in + ((size_t)s * Hq + head[k]) * D
+                                         : (kind[k] == 1 ? a.k_in : a.v_in) + ((size_t)s * Hkv + head[k]) * D;
+      load_words<W>(src, c1, x1[k]);
+      load_words<W>(src, c2, x2[k]);
+    }
+  }
+  if (t < HALF) {
+    const double pos = (double)a.prefix_lens[g] + (double)L;
+    double sn, cs;
+    sincos(pos * a.inv_freq[t], &sn, &cs);
+#pragma unroll
+    for (int set = 0; set < 2; ++set) {
+      const uint16_t* w = set == 0 ? a.q_norm_w : a.k_norm_w;
+      const double w1 = (double)__uint_as_float((uint32_t)w[t] << 16);
+      const double w2 = (double)__uint_as_float((uint32_t)w[t + HALF] << 16);
+      s_tab[set][0][t] = w1 * cs;
+      s_tab[set][1][t] = w2 * sn;
+      s_tab[set][2][t] = w2 * cs;
+      s_tab[set][3][t] = w1 * sn;
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < SPL; ++k) {
+    if (kind[k] < 3) prep_slot<D, FP8>(a, s, kind[k], head[k], l16, L, x1[k], x2[k], s_tab);
+  }
+}
+
+template <int D, int SPL>
+hipError_t launch_d(QkPrepArgs a, bool fp8, hipStream_t stream) {
+  a.blocks_per_seq = cdiv(a.num_q_heads + 2 * a.num_kv_heads, kGroups * SPL);
   const dim3 grid((unsigned)((long long)a.num_seqs * a.blocks_per_seq)), block(kPrepThreads);
-  if (fp8) qk_prep_kernel<D, true><<<grid, block, 0, stream>>>(a);
-  else qk_prep_kernel<D, false><<<grid, block, 0, stream>>>(a);
+  if (fp8) qk_prep_kernel<D, true, SPL><<<grid, block, 0, stream>>>(a);
+  else qk_prep_kernel<D, false, SPL><<<grid, block, 0, stream>>>(a);
   return hipGetLastError();
 }
 
 }  // namespace
 
-// Small batches split a sequence's heads over blocks of one head per wave
-// (more blocks in flight); from 1024 sequences on, one block per sequence
-// computes the angles once for all of its heads.
+// Small batches give each 16-lane group one slot (more blocks in flight);
+// from 1024 sequences on, two slots, so that a block covers 32 slots and
+// computes its sequence's tables once for twice the work.
 hipError_t launch_qk_prep(QkPrepArgs a, int head_dim, bool fp8, hipStream_t stream) {
   if (a.num_seqs <= 0) return hipSuccess;
-  const int heads = a.num_q_heads + a.num_kv_heads;
-  a.blocks_per_seq = a.num_seqs >= 1024 ? 1 : cdiv(heads, kPrepWaves);
-  a.heads_per_block = cdiv(heads, a.blocks_per_seq);
-  if (head_dim == 128) return launch_d<128>(a, fp8, stream);
-  if (head_dim == 64) return launch_d<64>(a, fp8, stream);
+  const bool two = a.num_seqs >= 1024;
+  if (head_dim == 128) return two ? launch_d<128, 2>(a, fp8, stream) : launch_d<128, 1>(a, fp8, stream);
+  if (head_dim == 64) return two ? launch_d<64, 2>(a, fp8, stream) : launch_d<64, 1>(a, fp8, stream);
   return hipErrorInvalidValue;
 }
 

@@ -87,7 +87,7 @@ CASES = [
     ("ragged-d64", [0, 1, 1, 0], [33, 2], [5, 0, 64, 9], 4, 2, 64, "bf16", 1.0, 1.0),
     ("mha-d64", [0, 0, 0], [12], [3, 16, 17], 4, 4, 64, "bf16", 1.0, 1.0),
     ("fp8-requant", [0, 0, 1, 1, 1], [20, 40], [0, 5, 15, 16, 33], 16, 8, 128, "fp8", 4.0, 0.25),
-    ("fp8-keep", [0, 0, 1, 1], [20, 40], [3, 7, 9, 30], 16, 8, 128, "fp8", 0.25, 4.0),
+    ("fp8-keep", [0, 0, 1, 1], [20, 40], [3, 7, 9, 30], 16, 8, 128, "fp8", 0.25, 8.0),
     ("fp8-d64", [0, 1, 0, 1], [8, 100], [1, 2, 17, 63], 8, 2, 64, "fp8", 2.0, 0.5),
 ]
 
