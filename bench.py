@@ -16,6 +16,11 @@ group's prompt-prefix K/V once (for groups with live members), every
 sequence's response K/V (including an appended token), q, out and lse, plus for
 an append the new k/v read and written, plus 8 bytes of fp8 scales per
 (page, kv-head) read. Plan, partial results and block tables are overhead.
+
+Other modes, each printing its own JSON line: --prefill (the shared-prefix
+prefill of the workload's prompts) and --fgd (the whole decode step from the
+raw projections, q/k prep included, at the frontier operating point of 2
+groups x 8 live samples).
 """
 import argparse
 import hashlib
