@@ -16,6 +16,8 @@ Everything is computed in float64 from the plain definitions:
   the one-time write of its K/V pages;
 * the pre-attention side of a decode step: RMS norm and rotary embedding of
   q and k, then the append;
+* one rollout round under Slime, CGP and CGP+FGD scheduling, simulated one
+  decode step at a time (``sched``);
 * bf16 and OCP e4m3fn decoding from the formats' bit definitions.
 
 Every function here is pinned by ``-m "not gpu"`` tests against library
@@ -27,8 +29,10 @@ from .combine import lse_combine
 from .append import kv_append, append_for_workload
 from .prefill import prefill_attention, prefill_kv_write
 from .qkprep import decode_positions, decode_step_prep, qk_prep, rms_norm, rope
+from .sched import simulate as simulate_schedule
 
 __all__ = ["bf16_to_f64", "bf16_to_f32", "e4m3_to_f64", "e4m3_encode", "E4M3_MAX",
            "decode_attention", "key_slots", "attention_for_workload",
            "lse_combine", "kv_append", "append_for_workload", "prefill_attention", "prefill_kv_write",
-           "decode_positions", "decode_step_prep", "qk_prep", "rms_norm", "rope"]
+           "decode_positions", "decode_step_prep", "qk_prep", "rms_norm", "rope",
+           "simulate_schedule"]
