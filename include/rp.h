@@ -280,6 +280,78 @@ rp_status rp_plan_layout(const rp_paged_kv* kv, const rp_group_layout* layout, r
 rp_status rp_validate_layout(const rp_paged_kv* kv, const rp_group_layout* layout,
                              hipStream_t stream);
 
+/* ---- Scheduling simulation (host) -------------------------------------
+ * One rollout round and its training under the paper's schedulers (Sections
+ * 3.2-3.3, Eq. 2-6, Algorithm 1). All pointers here are HOST pointers; the
+ * call is synchronous and touches no GPU.
+ *
+ * Rollout node: R groups of K requests; request q = g K + i belongs to group
+ * g (submission order = g) and generates resp_lens[q] >= 1 tokens after its
+ * group's prompt of prompt_lens[g] >= 0 tokens. At each scheduling cycle (a
+ * decode-step boundary): under RP_SCHED_CGP_FGD, while the frontier holds
+ * fewer than frontier_width groups, the lowest-order group not yet admitted
+ * joins it and its K requests join the admitted queue (Eq. 5-6); under the
+ * other modes all R K requests are in that queue from the start, group by
+ * group. Then admitted requests enter the running set, first come first
+ * served, while it holds fewer than max_running; the first request of a group
+ * to run brings the group's prompt prefill into that step. A decode step
+ * lasts step_base + step_per_seq n + step_per_ctx_token ctx + prefill, with n
+ * running requests, ctx the sum of their prompt plus generated tokens before
+ * the step, prefill the sum of prefill_per_token prompt_lens[g] over the
+ * groups started in that cycle; every running request generates one token.
+ * A group is serving-complete at the end of the step in which its last
+ * request finishes, and leaves the frontier.
+ * Control node: the group is trainable-complete mat_base + mat_per_token
+ * (its response tokens) later and joins the trainer FIFO (by time, ties by
+ * group order).
+ * Training node: update k consumes FIFO entries kU .. kU+U-1 (U =
+ * update_groups, which must divide R) and lasts the sum over its groups of
+ * train_base + train_per_token (K prompt + response tokens of the group),
+ * plus opt_step. It starts when the trainer is free and the U-th of those
+ * groups is trainable (CGP modes) or every group is (RP_SCHED_SLIME), Eq. 2.
+ * Sums are accumulated in the order written here, in IEEE double without
+ * contraction, so results are reproducible bit for bit.
+ * Cost parameters must be finite and >= 0 (seconds). */
+typedef enum {
+  RP_SCHED_SLIME = 0,    /* train after the whole rollout is trainable */
+  RP_SCHED_CGP = 1,      /* complete-group pipelining, request-level FIFO admission */
+  RP_SCHED_CGP_FGD = 2   /* complete-group pipelining with frontier-group dispatch */
+} rp_sched_mode;
+
+typedef struct {
+  rp_sched_mode mode;
+  int32_t num_groups;      /* R */
+  int32_t group_size;      /* K */
+  int32_t update_groups;   /* U = B / K, divides R */
+  int32_t frontier_width;  /* F_w (RP_SCHED_CGP_FGD only, >= 1) */
+  int32_t max_running;     /* engine concurrency, >= 1 */
+  double step_base, step_per_seq, step_per_ctx_token, prefill_per_token;
+  double mat_base, mat_per_token;
+  double train_base, train_per_token, opt_step;
+} rp_sched_config;
+
+typedef struct {
+  double t_first_u;    /* the first U groups are all trainable (the U-th FIFO entry) */
+  double t_complete;   /* every group trainable */
+  double t_start;      /* first update starts (Eq. 2) */
+  double delta_cgp;    /* t_complete - t_first_u (Eq. 3) */
+  double t_train_end;  /* last update ends; rollout starts at 0 */
+  double compute;      /* summed update durations */
+  double wait;         /* trainer idle time in [0, t_train_end] */
+  double w_train;      /* t_start / t_train_end (Eq. 4) */
+  double wait_ratio;   /* wait / (wait + compute), the trainer-side ratio */
+  int64_t steps;       /* decode steps of the round */
+} rp_sched_summary;
+
+/* prompt_lens[R], resp_lens[R K] (host int32). summary is required; the
+ * per-group outputs may be NULL: serve_done[R], frontier_enter[R] (0 unless
+ * RP_SCHED_CGP_FGD), trainable[R] (double seconds), fifo[R] (group ids in
+ * FIFO order), update_start[R / U], update_end[R / U]. */
+rp_status rp_sched_simulate(const rp_sched_config* config, const int32_t* prompt_lens,
+                            const int32_t* resp_lens, rp_sched_summary* summary,
+                            double* serve_done, double* frontier_enter, double* trainable,
+                            int32_t* fifo, double* update_start, double* update_end);
+
 #ifdef __cplusplus
 }
 #endif

@@ -28,7 +28,8 @@ RP_KV_FP8_E4M3 = 1
 EXPORTED = ("rp_status_string", "rp_last_error", "rp_kv_append",
             "rp_group_decode_attn_workspace_size", "rp_group_decode_attn", "rp_lse_combine",
             "rp_plan", "rp_attn_parts", "rp_combine_parts", "rp_plan_layout", "rp_validate_layout",
-            "rp_prefill_kv_write", "rp_prefill_attn", "rp_decode_qk_prep")
+            "rp_prefill_kv_write", "rp_prefill_attn", "rp_decode_qk_prep", "rp_sched_simulate")
+RP_SCHED_MODES = {"slime": 0, "cgp": 1, "cgp_fgd": 2}
 
 
 class RpPagedKV(ctypes.Structure):
@@ -58,6 +59,21 @@ class RpPlanInfo(ctypes.Structure):
     _fields_ = [(n, ctypes.c_size_t) for n in ("hdr", "grp_off", "grp_members", "prefix_items", "resp_items",
                                                  "seq_parts", "part_o", "part_lse")] + \
                [(n, ctypes.c_int32) for n in ("max_prefix_items", "max_resp_items", "parts_per_row", "max_parts")]
+
+
+class RpSchedConfig(ctypes.Structure):
+    _fields_ = [("mode", ctypes.c_int32), ("num_groups", ctypes.c_int32), ("group_size", ctypes.c_int32),
+                ("update_groups", ctypes.c_int32), ("frontier_width", ctypes.c_int32),
+                ("max_running", ctypes.c_int32)] + \
+               [(n, ctypes.c_double) for n in ("step_base", "step_per_seq", "step_per_ctx_token", "prefill_per_token",
+                                                "mat_base", "mat_per_token", "train_base", "train_per_token",
+                                                "opt_step")]
+
+
+class RpSchedSummary(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_double) for n in ("t_first_u", "t_complete", "t_start", "delta_cgp", "t_train_end",
+                                                "compute", "wait", "w_train", "wait_ratio")] + \
+               [("steps", ctypes.c_int64)]
 
 
 class RpError(RuntimeError):
@@ -93,6 +109,7 @@ def load() -> ctypes.CDLL:
         "rp_prefill_kv_write": (ctypes.c_int, [P, P, P, P, P]),
         "rp_prefill_attn": (ctypes.c_int, [P, P, P, P, P, F32, P, P, P]),
         "rp_decode_qk_prep": (ctypes.c_int, [P, P, P, P, P, P, P, ctypes.c_double, ctypes.c_double, P, P, P]),
+        "rp_sched_simulate": (ctypes.c_int, [P, P, P, P, P, P, P, P, P, P]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -237,3 +254,29 @@ def prefill_kv_write(kv, layout, k, v, stream=None) -> None:
 def prefill_attn(kv, layout, q, k, v, softmax_scale, out, lse, stream=None) -> None:
     _check(load().rp_prefill_attn(ctypes.byref(kv), ctypes.byref(layout), _ptr(q), _ptr(k), _ptr(v),
                                   float(softmax_scale), _ptr(out), _ptr(lse), _stream(stream)), "rp_prefill_attn")
+
+
+def sched_simulate(*, mode, group_size, update_groups, prompt_lens, resp_lens, max_running, frontier_width=0,
+                   step_base=0.0, step_per_seq=0.0, step_per_ctx_token=0.0, prefill_per_token=0.0,
+                   mat_base=0.0, mat_per_token=0.0, train_base=0.0, train_per_token=0.0, opt_step=0.0) -> dict:
+    """Run rp_sched_simulate on host arrays; returns the summary and the per-group timelines."""
+    import numpy as np
+    prompt = np.ascontiguousarray(prompt_lens, dtype=np.int32)
+    resp = np.ascontiguousarray(resp_lens, dtype=np.int32)
+    R = int(prompt.shape[0])
+    U = max(int(update_groups), 1)
+    cfg = RpSchedConfig(RP_SCHED_MODES[mode], R, int(group_size), int(update_groups), int(frontier_width),
+                        int(max_running), step_base, step_per_seq, step_per_ctx_token, prefill_per_token,
+                        mat_base, mat_per_token, train_base, train_per_token, opt_step)
+    summ = RpSchedSummary()
+    f64 = [np.zeros(R, np.float64) for _ in range(3)]
+    fifo = np.zeros(R, np.int32)
+    upd = [np.zeros(max(R // U, 1), np.float64) for _ in range(2)]
+    dp = lambda a: a.ctypes.data_as(ctypes.c_void_p)
+    _check(load().rp_sched_simulate(ctypes.byref(cfg), dp(prompt), dp(resp), ctypes.byref(summ), dp(f64[0]),
+                                    dp(f64[1]), dp(f64[2]), dp(fifo), dp(upd[0]), dp(upd[1])),
+           "rp_sched_simulate")
+    out = {n: getattr(summ, n) for n, _ in RpSchedSummary._fields_}
+    out.update(serve_done=f64[0].tolist(), frontier_enter=f64[1].tolist(), trainable=f64[2].tolist(),
+               fifo=fifo.tolist(), update_start=upd[0][:R // U].tolist(), update_end=upd[1][:R // U].tolist())
+    return out

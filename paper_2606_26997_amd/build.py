@@ -13,6 +13,8 @@ BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "librp.so")
 SOURCES = ["rp_api.hip", "rp_plan.hip", "rp_attn.hip", "rp_combine.hip", "rp_append.hip", "rp_prefill.hip",
            "rp_qkprep.hip"]
+# Host-only C++ (no device code), built with the system compiler.
+HOST_SOURCES = ["rp_sched.cpp"]
 ARCH = "gfx950"
 
 # Packed-fp32 VALU instructions are disabled for all device code. MFMA
@@ -23,6 +25,8 @@ HIPCC_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Wall",
                "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
                "-mllvm", "-amdgpu-mfma-vgpr-form",
                "-I", INCLUDE, "-I", CSRC]
+# The scheduling simulation promises bit-reproducible sums: no contraction.
+HOST_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-Wall", "-ffp-contract=off", "-I", INCLUDE, "-I", CSRC]
 
 
 def hipcc() -> str:
@@ -52,8 +56,13 @@ def build(verbose: bool = False) -> str:
             print(out, file=sys.stderr)
         return obj
 
-    with ThreadPoolExecutor(max_workers=min(len(SOURCES), os.cpu_count() or 1)) as ex:
-        objs = list(ex.map(compile_one, SOURCES))
+    def compile_host(src):
+        obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
+        _run([shutil.which("g++") or "g++", *HOST_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj])
+        return obj
+
+    with ThreadPoolExecutor(max_workers=min(len(SOURCES) + len(HOST_SOURCES), os.cpu_count() or 1)) as ex:
+        objs = list(ex.map(compile_one, SOURCES)) + list(ex.map(compile_host, HOST_SOURCES))
     tmp = LIB + ".tmp"
     _run([cc, "-shared", "-fPIC", f"--offload-arch={ARCH}", *objs, "-o", tmp])
     os.replace(tmp, LIB)

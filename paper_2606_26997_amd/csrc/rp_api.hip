@@ -534,3 +534,11 @@ rp_status rp_validate_layout(const rp_paged_kv* kv, const rp_group_layout* l, hi
 }
 
 }  // extern "C"
+
+namespace rp {
+rp_status set_error(rp_status st, const char* msg) {
+  snprintf(g_err, sizeof(g_err), "%s", msg);
+  return st;
+}
+void clear_error() { g_err[0] = 0; }
+}  // namespace rp
