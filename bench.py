@@ -18,9 +18,10 @@ an append the new k/v read and written, plus 8 bytes of fp8 scales per
 (page, kv-head) read. Plan, partial results and block tables are overhead.
 
 Other modes, each printing its own JSON line: --prefill (the shared-prefix
-prefill of the workload's prompts) and --fgd (the whole decode step from the
+prefill of the workload's prompts), --fgd (the whole decode step from the
 raw projections, q/k prep included, at the frontier operating point of 2
-groups x 8 live samples).
+groups x 8 live samples) and --sim (rollout rounds under Slime, CGP and
+CGP+FGD, simulated with decode-step costs measured on the GPU).
 """
 import argparse
 import hashlib
@@ -59,6 +60,9 @@ def parse_args():
     p.add_argument("--fgd", action="store_true",
                    help="time the whole decode step (q/k norm + rotary + append, plan, attention, combine) at "
                         "the frontier operating point: 2 groups x 8 live samples")
+    p.add_argument("--sim", action="store_true",
+                   help="simulate rollout rounds under Slime, CGP and CGP+FGD with decode-step costs measured "
+                        "on this GPU")
     p.add_argument("--traffic-from", metavar="DIR", default=None,
                    help="summarise rocprofv3 --pmc runs under DIR (pmc_fetch, pmc_write, pmc_copy_fetch, "
                         "pmc_copy_write) into the stored HBM traffic of the partial-attention kernel")
@@ -357,6 +361,188 @@ def fgd_bench(args):
     print(json.dumps(line), flush=True)
 
 
+# Qwen3-1.7B: 28 layers, 8 kv-heads of 128 channels; 1.7e9 parameters.
+QWEN3_LAYERS, QWEN3_PARAMS = 28, 1.7e9
+KV_BYTES_PER_TOKEN = QWEN3_LAYERS * 8 * 128 * 2 * 2       # bf16 K and V of one token, all layers
+GEMM_FLOPS = 0.5 * 2.5e15                                  # assumed: projections and MLP at half the bf16 peak
+PAPER_TRAIN_R96 = 587.4                                    # trainer compute, LSAT-AR, R = 96, Slime (Table 1)
+PAPER_ROLLOUT_R96 = 525.0                                  # mid-range of Slime's first dispatch at R = 96 (509-543 s)
+
+
+def _measure_decode_layer(args, rng):
+    """Per-layer decode-step time (q/k prep + plan + attention + combine) at several batch shapes,
+    fitted as a + b * sequences + c * context tokens (context counted per sequence, prompt included)."""
+    import numpy as np
+    import torch
+    import paper_2606_26997_amd as rp
+    from workloads import make_qkprep_inputs, make_workload
+    rows, times = [], []
+    for S, rmax in ((16, 6016), (64, 6016), (256, 6016), (64, 2000), (256, 12000)):
+        resp = rng.integers(0, rmax + 1, S)
+        wl = make_workload(num_q_heads=16, num_kv_heads=8, head_dim=128, seq_to_group=np.arange(S) // 8,
+                           prefix_lens=np.full(S // 8, 512), resp_lens=resp, seed=int(S + rmax), append=True,
+                           k_mult=0.5, rng=rng)
+        x = make_qkprep_inputs(num_seqs=S, num_q_heads=16, num_kv_heads=8, head_dim=128, seed=S)
+        b = rp.DeviceBatch.from_workload(wl, device="cuda:0")
+        b.set_projections(x.q_in, x.k_in, x.v_in, x.q_norm_w, x.k_norm_w)
+        for _ in range(10):
+            b.decode_step()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(50):
+            b.decode_step()
+        torch.cuda.synchronize()
+        times.append((time.perf_counter() - t0) / 50)
+        rows.append([1.0, S, float(512 * S + resp.sum() + S)])
+        del b
+    coef, *_ = np.linalg.lstsq(np.array(rows), np.array(times), rcond=None)
+    return [float(c) for c in coef], [dict(seqs=int(r[1]), ctx_tokens=int(r[2]), us=round(t * 1e6, 2))
+                                      for r, t in zip(rows, times)]
+
+
+def _measure_prefill_token():
+    """Per-layer prefill time per prompt token (page write + causal attention), 32 prompts of 600 tokens."""
+    import numpy as np
+    import torch
+    import paper_2606_26997_amd as rp
+    from workloads import make_prefill_workload
+    w = make_prefill_workload(num_q_heads=16, num_kv_heads=8, head_dim=128, prefix_lens=[600] * 32, seed=5)
+    b = rp.PrefillBatch.from_workload(w, device="cuda:0")
+    for _ in range(5):
+        b.step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(20):
+        b.step()
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) / 20 / w.num_tokens
+
+
+def _measure_weight_read():
+    """Time to read the model's weight bytes once from HBM (what a small-batch decode step pays)."""
+    import torch
+    w = torch.ones(int(QWEN3_PARAMS), dtype=torch.bfloat16, device="cuda:0")
+    for _ in range(3):
+        w.sum()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(10):
+        w.sum()
+    torch.cuda.synchronize()
+    el = (time.perf_counter() - t0) / 10
+    del w
+    return el
+
+
+def sim_bench(args):
+    """Rollout rounds of R groups x K = 8 under Slime, CGP and CGP+FGD (U = 2, F_w = 2), simulated by
+    rp_sched_simulate with decode-step costs measured on this GPU."""
+    import numpy as np
+    import torch
+    import paper_2606_26997_amd as rp
+    import oracle
+    from workloads import make_rollout_workload
+
+    torch.cuda.set_device(0)
+    rng = np.random.default_rng(77 if args.seed is None else args.seed)
+    (a, b, c), points = _measure_decode_layer(args, rng)
+    pre_tok = _measure_prefill_token()
+    t_w = _measure_weight_read()
+    per_tok_gemm = 2 * QWEN3_PARAMS / GEMM_FLOPS
+    cost = dict(step_base=QWEN3_LAYERS * max(a, 0.0) + t_w, step_per_seq=QWEN3_LAYERS * max(b, 0.0) + per_tok_gemm,
+                step_per_ctx_token=QWEN3_LAYERS * max(c, 0.0), prefill_per_token=QWEN3_LAYERS * pre_tok + per_tok_gemm)
+    K, U, Fw, P_MAX, CAP = 8, 2, 2, 1024, 8192
+
+    # Concurrency from the KV memory left after the weights, at the average context of a request
+    # (prompt plus response), as a serving engine admits against current usage.
+    P96, L96 = make_rollout_workload(num_groups=96, group_size=K, seed=96, prompt_max=P_MAX, resp_cap=CAP)
+    avg_ctx = float(P96.mean() + L96.mean())
+
+    def capacity(hbm_bytes):
+        return int((0.9 * hbm_bytes - 2 * QWEN3_PARAMS) // (KV_BYTES_PER_TOKEN * avg_ctx))
+
+    def rounds(scale, cap):
+        out = {}
+        for R in (32, 64, 96):
+            P, L = make_rollout_workload(num_groups=R, group_size=K, seed=R, prompt_max=P_MAX, resp_cap=CAP)
+            # Trainer speed from the paper's trainer compute at R = 96, per trained token.
+            P96, L96 = make_rollout_workload(num_groups=96, group_size=K, seed=96, prompt_max=P_MAX, resp_cap=CAP)
+            tpt = PAPER_TRAIN_R96 / float(K * P96.astype(np.int64).sum() + L96.astype(np.int64).sum())
+            kw = dict(group_size=K, update_groups=U, prompt_lens=P, resp_lens=L, max_running=cap, frontier_width=Fw,
+                      mat_base=1.0, train_per_token=tpt, **{k: v * scale for k, v in cost.items()})
+            res = {m: rp.sched_simulate(mode=m, **kw) for m in ("slime", "cgp", "cgp_fgd")}
+            sl = res["slime"]["t_train_end"]
+            out[f"R{R}"] = {m: dict(train_end_s=round(r["t_train_end"], 2),
+                                    reduction_vs_slime_pct=round(100 * (1 - r["t_train_end"] / sl), 2),
+                                    first_dispatch_s=round(r["t_start"], 2), rollout_s=round(r["t_complete"], 2),
+                                    w_train=round(r["w_train"], 4), wait_ratio=round(r["wait_ratio"], 4))
+                            for m, r in res.items()}
+            out[f"R{R}"]["fgd_gain_over_cgp_pct"] = round(
+                100 * (1 - res["cgp_fgd"]["t_train_end"] / res["cgp"]["t_train_end"]), 2)
+        return out
+
+    cap_mi355x, cap_a100 = capacity(288e9), capacity(2 * 40e9)
+    mi = rounds(1.0, cap_mi355x)
+    # The paper's rollout regime: the same cost model slowed down until Slime's R = 96 rollout
+    # ends where the paper's first dispatch does, with the KV capacity of 2 x A100 40 GB.
+    base = rp.sched_simulate(mode="slime", group_size=K, update_groups=U, prompt_lens=P96, resp_lens=L96,
+                             max_running=cap_a100, **cost)
+    alpha = PAPER_ROLLOUT_R96 / max(base["serve_done"])
+    paper = rounds(alpha, cap_a100)
+
+    # Frontier width against the trainer's supply, R = 96, both regimes.
+    tpt96 = PAPER_TRAIN_R96 / float(K * P96.astype(np.int64).sum() + L96.astype(np.int64).sum())
+    sweep = {}
+    for name, scale, cap in (("mi355x_rollout", 1.0, cap_mi355x), ("paper_regime", alpha, cap_a100)):
+        sweep[name] = {}
+        for fw in (2, 4, 8, 16):
+            r = rp.sched_simulate(mode="cgp_fgd", group_size=K, update_groups=U, prompt_lens=P96, resp_lens=L96,
+                                  max_running=cap, frontier_width=fw, mat_base=1.0, train_per_token=tpt96,
+                                  **{k: v * scale for k, v in cost.items()})
+            sweep[name][f"Fw{fw}"] = dict(train_end_s=round(r["t_train_end"], 2), first_dispatch_s=round(r["t_start"], 2),
+                                         rollout_s=round(r["t_complete"], 2), wait_ratio=round(r["wait_ratio"], 4))
+
+    # Speed of the native simulation against the step-by-step oracle, same round.
+    kw = dict(group_size=K, update_groups=U, prompt_lens=P96, resp_lens=L96, max_running=cap_a100, frontier_width=Fw,
+              **{k: v * alpha for k, v in cost.items()})
+    t0 = time.perf_counter()
+    for _ in range(20):
+        rp.sched_simulate(mode="cgp_fgd", **kw)
+    native_s = (time.perf_counter() - t0) / 20
+    t0 = time.perf_counter()
+    ref = oracle.simulate_schedule(mode="cgp_fgd", **kw)
+    oracle_s = time.perf_counter() - t0
+    assert ref["t_train_end"] == rp.sched_simulate(mode="cgp_fgd", **kw)["t_train_end"]
+
+    val = mi["R96"]["cgp_fgd"]["reduction_vs_slime_pct"]
+    line = {
+        "metric": "simulated rollout-to-train-end reduction of CGP+FGD vs Slime (R=96, K=8, U=2, F_w=2), "
+                  "decode-step costs measured on MI355X",
+        "value": val, "unit": "%", "n_gpus": 1, "steps": None, "warmup": None, "ms_per_step": None,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f64", "data": "synthetic",
+        "config": {"workload": "rollout rounds of R = 32/64/96 groups x 8 samples, prompts U[128, 1024], "
+                               "responses lognormal (median 3000; group sigma 0.5, sample sigma 0.3; cap 8192)",
+                   "max_running_mi355x": cap_mi355x, "max_running_2xA100": cap_a100},
+        "cost_model": {k: float(f"{v:.6g}") for k, v in cost.items()},
+        "measured": {"decode_layer_fit_us": {"base": round(a * 1e6, 3), "per_seq": round(b * 1e6, 5),
+                                             "per_ctx_token": round(c * 1e6, 8)},
+                     "decode_layer_points": points, "prefill_layer_us_per_token": round(pre_tok * 1e6, 5),
+                     "weight_read_ms": round(t_w * 1e3, 4)},
+        "assumed": {"gemm_flops": GEMM_FLOPS, "materialise_s_per_group": 1.0,
+                    "trainer_s_per_token_from_paper_R96": PAPER_TRAIN_R96},
+        "mi355x_rollout": mi,
+        "paper_regime": {"rollout_slowdown": round(alpha, 3), **paper},
+        "frontier_width_sweep_R96": sweep,
+        "paper_context": {"reduction_vs_slime_pct_R96": [39.8, 42.3], "first_dispatch_s_R96_cgp": [46, 90],
+                          "first_dispatch_s_R96_cgp_fgd": [52, 61], "wait_ratio_R96_pct": [13.8, 15.0],
+                          "fgd_gain_over_cgp_pct": [2.5, 11.4]},
+        "simulator_s_per_round": round(native_s, 6),
+        "cpu_baseline": {"value": round(oracle_s, 3), "unit": "s per round", "cores": 1, "kind": "oracle",
+                         "sample": "the same R = 96 CGP+FGD round, simulated one decode step at a time"},
+    }
+    print(json.dumps(line), flush=True)
+
+
 def main():
     args = parse_args()
     if args.gpus != 1:
@@ -378,6 +564,9 @@ def main():
         return
     if args.fgd:
         fgd_bench(args)
+        return
+    if args.sim:
+        sim_bench(args)
         return
 
     import paper_2606_26997_amd as rp
