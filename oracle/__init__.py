@@ -18,6 +18,7 @@ Everything is computed in float64 from the plain definitions:
   q and k, then the append;
 * one rollout round under Slime, CGP and CGP+FGD scheduling, simulated one
   decode step at a time (``sched``);
+* GRPO group statistics and advantages (Eq. 1, ``grpo``);
 * bf16 and OCP e4m3fn decoding from the formats' bit definitions.
 
 Every function here is pinned by ``-m "not gpu"`` tests against library
@@ -30,9 +31,10 @@ from .append import kv_append, append_for_workload
 from .prefill import prefill_attention, prefill_kv_write
 from .qkprep import decode_positions, decode_step_prep, qk_prep, rms_norm, rope
 from .sched import simulate as simulate_schedule
+from .grpo import advantage, advantage_f32, group_stats
 
 __all__ = ["bf16_to_f64", "bf16_to_f32", "e4m3_to_f64", "e4m3_encode", "E4M3_MAX",
            "decode_attention", "key_slots", "attention_for_workload",
            "lse_combine", "kv_append", "append_for_workload", "prefill_attention", "prefill_kv_write",
            "decode_positions", "decode_step_prep", "qk_prep", "rms_norm", "rope",
-           "simulate_schedule"]
+           "simulate_schedule", "advantage", "advantage_f32", "group_stats"]
