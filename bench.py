@@ -20,8 +20,9 @@ an append the new k/v read and written, plus 8 bytes of fp8 scales per
 Other modes, each printing its own JSON line: --prefill (the shared-prefix
 prefill of the workload's prompts), --fgd (the whole decode step from the
 raw projections, q/k prep included, at the frontier operating point of 2
-groups x 8 live samples) and --sim (rollout rounds under Slime, CGP and
-CGP+FGD, simulated with decode-step costs measured on the GPU).
+groups x 8 live samples), --sim (rollout rounds under Slime, CGP and
+CGP+FGD, simulated with decode-step costs measured on the GPU) and --grpo (the
+GRPO group advantages of Eq. 1).
 """
 import argparse
 import hashlib
@@ -63,6 +64,8 @@ def parse_args():
     p.add_argument("--sim", action="store_true",
                    help="simulate rollout rounds under Slime, CGP and CGP+FGD with decode-step costs measured "
                         "on this GPU")
+    p.add_argument("--grpo", action="store_true",
+                   help="time the GRPO group advantages (Eq. 1) for a paper-size round and a large batch")
     p.add_argument("--traffic-from", metavar="DIR", default=None,
                    help="summarise rocprofv3 --pmc runs under DIR (pmc_fetch, pmc_write, pmc_copy_fetch, "
                         "pmc_copy_write) into the stored HBM traffic of the partial-attention kernel")
@@ -543,6 +546,48 @@ def sim_bench(args):
     print(json.dumps(line), flush=True)
 
 
+def grpo_bench(args):
+    """GRPO advantages (Eq. 1): one round of the paper (R = 96 groups of K = 8) and 2^22 groups of 8."""
+    import numpy as np
+    import torch
+    import paper_2606_26997_amd as rp
+
+    torch.cuda.set_device(0)
+    res = {}
+    for name, R in (("round_R96", 96), ("batch_2^22", 1 << 22)):
+        K = 8
+        r = torch.from_numpy(np.random.default_rng(R).standard_normal((R, K)).astype(np.float32)).cuda()
+        adv = torch.empty_like(r)
+        mu = torch.empty(R, dtype=torch.float32, device="cuda")
+        sd = torch.empty(R, dtype=torch.float32, device="cuda")
+        for _ in range(args.warmup):
+            rp.grpo_advantage(r, adv, mu, sd)
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+        for a, b in ev:
+            a.record()
+            rp.grpo_advantage(r, adv, mu, sd)
+            b.record()
+        torch.cuda.synchronize()
+        us = float(np.mean([a.elapsed_time(b) for a, b in ev])) * 1e3
+        nbytes = R * K * 4 * 2 + R * 8          # rewards read, advantages written, mean and std written
+        res[name] = dict(groups=R, group_size=K, us=round(us, 2), bytes=nbytes,
+                         GBps=round(nbytes / (us * 1e-6) / 1e9, 1))
+    big = res["batch_2^22"]
+    line = {
+        "metric": "GRPO group advantages (Eq. 1): achieved HBM GB/s on 2^22 groups of 8",
+        "value": big["GBps"], "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(big["us"] / 1e3, 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f64", "data": "synthetic",
+        "config": {"workload": "rewards N(0, 1) in groups of 8: 2^22 groups, and one round of 96 groups"},
+        "runs": res,
+        "roofline": {"kernel": "grpo_fixed_kernel<8>", "bound": "hbm", "achieved": big["GBps"], "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": round(big["GBps"] / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "algorithmic_bytes_per_launch": big["bytes"]},
+        "cpu_baseline": None,
+    }
+    print(json.dumps(line), flush=True)
+
+
 def main():
     args = parse_args()
     if args.gpus != 1:
@@ -567,6 +612,9 @@ def main():
         return
     if args.sim:
         sim_bench(args)
+        return
+    if args.grpo:
+        grpo_bench(args)
         return
 
     import paper_2606_26997_amd as rp

@@ -280,6 +280,23 @@ rp_status rp_plan_layout(const rp_paged_kv* kv, const rp_group_layout* layout, r
 rp_status rp_validate_layout(const rp_paged_kv* kv, const rp_group_layout* layout,
                              hipStream_t stream);
 
+/* ---- GRPO group statistics (Eq. 1) -----------------------------------
+ * For each of num_groups groups of group_size rewards r_1..r_K (fp32,
+ * rewards[g][i], device), in fp64:
+ *   mu = sum r / K,  sigma = sqrt(sum (r - mu)^2 / (K - ddof))  (0 when K - ddof < 1),
+ *   A_i = (r_i - mu) / (sigma + eps_std),
+ * each output rounded once to fp32: advantages[g][i], and, unless NULL,
+ * group_mean[g] = mu and group_std[g] = sigma. The paper fixes neither the
+ * estimator nor eps_std: ddof = 1 is the unbiased estimate (the default of
+ * common GRPO implementations), ddof = 0 the population one; eps_std must
+ * be finite and >= 0 (1e-6 is the usual choice). A group of equal rewards
+ * gets A = 0 when eps_std > 0 (NaN when eps_std = 0). Arrays are fp32 and 4-byte aligned (16-byte alignment of
+ * rewards and advantages enables vector loads for K = 4, 8, 16);
+ * advantages may alias rewards. */
+rp_status rp_grpo_advantage(const float* rewards, int32_t num_groups, int32_t group_size,
+                            double eps_std, int32_t ddof, float* advantages,
+                            float* group_mean, float* group_std, hipStream_t stream);
+
 /* ---- Scheduling simulation (host) -------------------------------------
  * One rollout round and its training under the paper's schedulers (Sections
  * 3.2-3.3, Eq. 2-6, Algorithm 1). All pointers here are HOST pointers; the

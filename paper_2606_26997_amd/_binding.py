@@ -28,7 +28,8 @@ RP_KV_FP8_E4M3 = 1
 EXPORTED = ("rp_status_string", "rp_last_error", "rp_kv_append",
             "rp_group_decode_attn_workspace_size", "rp_group_decode_attn", "rp_lse_combine",
             "rp_plan", "rp_attn_parts", "rp_combine_parts", "rp_plan_layout", "rp_validate_layout",
-            "rp_prefill_kv_write", "rp_prefill_attn", "rp_decode_qk_prep", "rp_sched_simulate")
+            "rp_prefill_kv_write", "rp_prefill_attn", "rp_decode_qk_prep", "rp_sched_simulate",
+            "rp_grpo_advantage")
 RP_SCHED_MODES = {"slime": 0, "cgp": 1, "cgp_fgd": 2}
 
 
@@ -110,6 +111,7 @@ def load() -> ctypes.CDLL:
         "rp_prefill_attn": (ctypes.c_int, [P, P, P, P, P, F32, P, P, P]),
         "rp_decode_qk_prep": (ctypes.c_int, [P, P, P, P, P, P, P, ctypes.c_double, ctypes.c_double, P, P, P]),
         "rp_sched_simulate": (ctypes.c_int, [P, P, P, P, P, P, P, P, P, P]),
+        "rp_grpo_advantage": (ctypes.c_int, [P, I32, I32, ctypes.c_double, I32, P, P, P, P]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -182,6 +184,14 @@ def decode_qk_prep(kv, layout, q_in, k_in, v_in, q_norm_w, k_norm_w, q_out, k_ou
                                     _ptr(q_norm_w), _ptr(k_norm_w), float(rms_eps), float(rope_theta),
                                     _ptr(q_out), _ptr(k_out), _stream(stream)),
            "rp_decode_qk_prep")
+
+
+def grpo_advantage(rewards, advantages, group_mean=None, group_std=None, *, eps_std=1e-6, ddof=1,
+                   stream=None) -> None:
+    """rewards, advantages: fp32 device tensors [R][K]; group_mean, group_std: [R] or None."""
+    R, K = int(rewards.shape[0]), int(rewards.shape[1])
+    _check(load().rp_grpo_advantage(_ptr(rewards), R, K, float(eps_std), int(ddof), _ptr(advantages),
+                                    _ptr(group_mean), _ptr(group_std), _stream(stream)), "rp_grpo_advantage")
 
 
 def group_decode_attn_workspace_size(kv: RpPagedKV, layout: RpGroupLayout) -> int:

@@ -394,6 +394,34 @@ rp_status rp_decode_qk_prep(const rp_paged_kv* kv, const rp_group_layout* l, con
   return e == hipSuccess ? RP_OK : hip_fail(e, "decode q/k prep kernel launch");
 }
 
+rp_status rp_grpo_advantage(const float* rewards, int32_t num_groups, int32_t group_size, double eps_std,
+                            int32_t ddof, float* advantages, float* group_mean, float* group_std,
+                            hipStream_t stream) {
+  g_err[0] = 0;
+  if (num_groups < 0 || group_size < 1)
+    return fail(RP_ERR_INVALID_ARG, "num_groups must be >= 0 and group_size >= 1");
+  if (ddof != 0 && ddof != 1) return fail(RP_ERR_INVALID_ARG, "ddof must be 0 or 1");
+  if (!(eps_std >= 0.0) || !std::isfinite(eps_std)) return fail(RP_ERR_INVALID_ARG, "eps_std must be finite and >= 0");
+  if ((long long)num_groups * group_size >= (1ll << 40)) return fail(RP_ERR_UNSUPPORTED, "too many rewards");
+  if (num_groups == 0) return RP_OK;
+  if (rewards == nullptr || advantages == nullptr || !aligned(rewards, 4) || !aligned(advantages, 4))
+    return fail(RP_ERR_INVALID_ARG, "rewards/advantages must be non-NULL fp32 arrays");
+  if ((group_mean != nullptr && !aligned(group_mean, 4)) || (group_std != nullptr && !aligned(group_std, 4)))
+    return fail(RP_ERR_INVALID_ARG, "group_mean/group_std must be fp32 arrays");
+  rp::GrpoArgs a;
+  a.rewards = rewards;
+  a.num_groups = num_groups;
+  a.group_size = group_size;
+  a.ddof = ddof;
+  a.eps_std = eps_std;
+  a.advantages = advantages;
+  a.mean = group_mean;
+  a.stdev = group_std;
+  a.vector_ok = aligned(rewards, 16) && aligned(advantages, 16);
+  hipError_t e = rp::launch_grpo(a, stream);
+  return e == hipSuccess ? RP_OK : hip_fail(e, "GRPO advantage kernel launch");
+}
+
 // Shared checks of the prefill calls; fills a (pointers of the projections
 // and outputs are checked by the callers).
 static rp_status prefill_args(const rp_paged_kv* kv, const rp_prefill_layout* l, rp::PrefillArgs* a, int* n_rep) {

@@ -78,6 +78,17 @@ struct AppendArgs {
   const void* v_new;
 };
 
+// GRPO advantages: rewards [num_groups][group_size] fp32.
+struct GrpoArgs {
+  const float* rewards;
+  int num_groups, group_size, ddof;
+  double eps_std;
+  float* advantages;  // [num_groups][group_size]
+  float* mean;        // [num_groups] or null
+  float* stdev;       // [num_groups] or null
+  bool vector_ok;     // rewards and advantages 16-byte aligned (group_size 4, 8 or 16 then loads float4)
+};
+
 constexpr int kMaxHeadDim = 128;
 
 // Pre-attention side of a decode step: q/k RMS norm + rotary embedding,
@@ -146,6 +157,7 @@ hipError_t launch_append(const AppendArgs& a, int head_dim, bool fp8, hipStream_
 hipError_t launch_prefill_kv_write(const PrefillArgs& a, int head_dim, bool fp8, hipStream_t stream);
 hipError_t launch_prefill_attn(const PrefillArgs& a, int head_dim, int n_rep, hipStream_t stream);
 hipError_t launch_qk_prep(QkPrepArgs a, int head_dim, bool fp8, hipStream_t stream);
+hipError_t launch_grpo(const GrpoArgs& a, hipStream_t stream);
 hipError_t launch_validate(const ValidateArgs& a, hipStream_t stream);
 
 }  // namespace rp

@@ -221,3 +221,18 @@ def test_decode_qk_prep_argument_checks():
     assert call(_kv(head_dim=96), lay) == rp.RP_ERR_UNSUPPORTED
     # An empty batch launches nothing and needs no pointers.
     assert call(kv, _layout(num_seqs=0), q=None, k=None, v=None, wq=None, wk=None, qo=None) == rp.RP_OK
+
+
+def test_grpo_advantage_argument_checks():
+    lib = rp.load()
+    call = lambda r=A, R=4, K=8, eps=1e-6, ddof=1, adv=A, mu=None, sd=None: \
+        lib.rp_grpo_advantage(r, R, K, eps, ddof, adv, mu, sd, None)
+    assert call(r=None) == rp.RP_ERR_INVALID_ARG and "rewards" in rp.last_error()
+    assert call(adv=A + 2) == rp.RP_ERR_INVALID_ARG
+    assert call(mu=A + 1) == rp.RP_ERR_INVALID_ARG and "group_mean" in rp.last_error()
+    assert call(K=0) == rp.RP_ERR_INVALID_ARG
+    assert call(R=-1) == rp.RP_ERR_INVALID_ARG
+    assert call(ddof=2) == rp.RP_ERR_INVALID_ARG and "ddof" in rp.last_error()
+    assert call(eps=-1e-6) == rp.RP_ERR_INVALID_ARG and "eps_std" in rp.last_error()
+    assert call(eps=float("inf")) == rp.RP_ERR_INVALID_ARG
+    assert call(R=0, r=None, adv=None) == rp.RP_OK
