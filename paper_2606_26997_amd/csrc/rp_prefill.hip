@@ -8,20 +8,17 @@
 // written rows (1 when amax = 0) and codes e4m3(x / scale), round to nearest
 // even, saturating.
 //
-// Causal attention: one wave per (group, kv-head, 16-row query tile). A tile
-// holds 16 / n_rep consecutive prompt tokens times the n_rep query heads that
-// share the kv-head, so the key blocks it reads serve all of them. Per 16-key
-// block: S^T = K Q^T on mfma 16x16x32 bf16, a causal mask on the diagonal,
-// an online softmax per row, O^T += V^T P^T on mfma 16x16x16 bf16 with V
-// staged through LDS; the next block's V is requested once this block's V is
-// staged and its K once the scores exist. K/V are read from the projections
-// (not from the pool), as the prompt's own attention needs no quantised copy.
+// Causal attention: a workgroup of 4 waves per (group, kv-head, block of
+// query rows); a 16-row tile holds 16 / n_rep consecutive prompt tokens times
+// the n_rep query heads that share the kv-head, so every key block serves all
+// of them (details at the kernel). K/V are read from the projections (not
+// from the pool), as the prompt's own attention needs no quantised copy.
 //
-// Grid: workgroup b takes (group, kv-head) pair b % NP and tile
-// max_tiles - 1 - b / NP (longest tiles, which see the most keys, first).
+// Grid: workgroup b takes (group, kv-head) pair b % NP and row block
+// max_blocks - 1 - b / NP (the last rows, which see the most keys, first).
 // Workgroups are dealt to the 8 XCDs round-robin, so with NP a multiple of 8
-// every tile of a pair runs on one XCD and re-reads the pair's K/V from that
-// XCD's L2.
+// every row block of a pair runs on one XCD and re-reads the pair's K/V from
+// that XCD's L2.
 #include "rp_device.h"
 #include "rp_internal.h"
 
@@ -107,169 +104,270 @@ __global__ __launch_bounds__(64) void prefill_kv_write_kernel(const PrefillArgs 
 // ---------------------------------------------------------------------------
 // Causal attention
 // ---------------------------------------------------------------------------
-// One 16-key block of kv-head h in flight (this lane's share): the A operand of
-// S^T = K Q^T (lane (r16, quad) holds key r16, columns kb*32 + quad*8 + 0..7)
-// and 16-byte pieces of the block's V rows for staging.
+// Workgroup of 4 waves on (group, kv-head) pair and a block of query rows:
+// wave w holds RT 16-row tiles (each 16 / n_rep consecutive prompt tokens
+// times the n_rep query heads of the kv-head), so a workgroup covers
+// 64 RT / n_rep tokens. Keys go through LDS in blocks of 32, double-buffered:
+// while the waves compute on one block, the next block's K (row-major) and V
+// (transposed, so that an MFMA operand of V^T is one 8-byte read) are loaded
+// from the projections and written into the other buffer; one barrier per
+// block. Per block and row tile: S^T = K Q^T on mfma 16x16x32 (Q stays in
+// registers), a causal mask, one online-softmax update per row, and
+// O^T += V^T P^T on mfma 16x16x16.
+constexpr int kPfWaves = 4;
+constexpr int kPfThreads = 64 * kPfWaves;
+constexpr int kKeyBlk = 32;
+
 template <int D>
-struct KeyBlock {
-  uint4 k[D / 32];
-  uint4 v[kPage * D * 2 / 1024];
+struct PfSmem {
+  static constexpr int kKPitch = D + 8;        // K rows, bf16 (16-byte aligned rows)
+  static constexpr int kVPitch = kKeyBlk + 4;  // V^T rows, bf16
+  static constexpr int kKElems = kKeyBlk * kKPitch;
+  static constexpr int kStage = kKElems + D * kVPitch;
+  static constexpr int kBytes = 2 * kStage * 2;
+  static constexpr int kKChunks = kKeyBlk * D / 8;          // 16-byte pieces of a K block
+  static constexpr int kVChunks = (kKeyBlk / 2) * (D / 8);  // (2 keys x 8 columns) pieces of a V block
+  static constexpr int kKPerThread = kKChunks / kPfThreads;
+  static_assert(kKChunks % kPfThreads == 0, "K block split");
+  static_assert(kVChunks <= kPfThreads, "V block split");
 };
 
-// Rows at or past the prompt's end are read from its last token (inside the
-// packed arrays) and masked where used.
+// This thread's share of one key block, in registers between the global
+// loads and the LDS writes. Clang vector types, not HIP's uint4: copies of
+// the latter go through memcpy and kept these values in scratch memory. Rows
+// at or past the prompt's end are read from its last token (inside the packed
+// arrays); their scores are masked.
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+struct PfBlock {
+  u32x4_t k0, k1, v0, v1;
+};
+
 template <int D>
-__device__ inline void load_block_k(const uint16_t* kbase, size_t pitch, int u0, int last, int lane, KeyBlock<D>& r) {
-  const int r16 = lane & 15, quad = lane >> 4;
-  const uint16_t* row = kbase + (size_t)min(u0 + r16, last) * pitch + quad * 8;
-#pragma unroll
-  for (int kb = 0; kb < D / 32; ++kb) r.k[kb] = *reinterpret_cast<const uint4*>(row + kb * 32);
-}
-template <int D>
-__device__ inline void load_block_v(const uint16_t* vbase, size_t pitch, int u0, int last, int lane, KeyBlock<D>& r) {
-#pragma unroll
-  for (int i = 0; i < kPage * D * 2 / 1024; ++i) {
-    const int e0 = i * 512 + lane * 8;
-    const int tok = e0 / D, col = e0 % D;
-    r.v[i] = *reinterpret_cast<const uint4*>(vbase + (size_t)min(u0 + tok, last) * pitch + col);
+__device__ inline void pf_load(const uint16_t* kbase, const uint16_t* vbase, size_t pitch, int u0, int last, int t,
+                               PfBlock& r) {
+  using L = PfSmem<D>;
+  static_assert(L::kKPerThread == 1 || L::kKPerThread == 2, "K pieces per thread");
+  {
+    const int key = t / (D / 8), col = (t - key * (D / 8)) * 8;
+    r.k0 = *reinterpret_cast<const u32x4_t*>(kbase + (size_t)min(u0 + key, last) * pitch + col);
+  }
+  if constexpr (L::kKPerThread == 2) {
+    const int c = t + kPfThreads;
+    const int key = c / (D / 8), col = (c - key * (D / 8)) * 8;
+    r.k1 = *reinterpret_cast<const u32x4_t*>(kbase + (size_t)min(u0 + key, last) * pitch + col);
+  }
+  if (L::kVChunks == kPfThreads || t < L::kVChunks) {
+    const int kp = t % (kKeyBlk / 2), d0 = (t / (kKeyBlk / 2)) * 8;
+    r.v0 = *reinterpret_cast<const u32x4_t*>(vbase + (size_t)min(u0 + 2 * kp, last) * pitch + d0);
+    r.v1 = *reinterpret_cast<const u32x4_t*>(vbase + (size_t)min(u0 + 2 * kp + 1, last) * pitch + d0);
   }
 }
 
-template <int D, int NREP>
-__global__ __launch_bounds__(64) void prefill_attn_kernel(const PrefillArgs a, int max_tiles) {
-  constexpr int KB = D / 32;        // MFMA k-blocks over head_dim
-  constexpr int DT = D / 16;        // 16-column output tiles
-  constexpr int STRIDE = D + 4;     // staged V row pitch (bf16)
-  constexpr int QSTRIDE = D + 8;    // query tile row pitch (bf16)
-  constexpr int TPT = 16 / NREP;    // prompt tokens per 16-row tile
-  __shared__ __attribute__((aligned(16))) uint16_t vt[kPage * STRIDE];
-  __shared__ __attribute__((aligned(16))) uint16_t qt[16 * QSTRIDE];
+template <int D>
+__device__ inline void pf_store(uint16_t* stage, int t, const PfBlock& r) {
+  using L = PfSmem<D>;
+  {
+    const int key = t / (D / 8), col = (t - key * (D / 8)) * 8;
+    *reinterpret_cast<u32x4_t*>(stage + key * L::kKPitch + col) = r.k0;
+  }
+  if constexpr (L::kKPerThread == 2) {
+    const int c = t + kPfThreads;
+    const int key = c / (D / 8), col = (c - key * (D / 8)) * 8;
+    *reinterpret_cast<u32x4_t*>(stage + key * L::kKPitch + col) = r.k1;
+  }
+  if (L::kVChunks == kPfThreads || t < L::kVChunks) {
+    const int kp = t % (kKeyBlk / 2), d0 = (t / (kKeyBlk / 2)) * 8;
+    uint16_t* vt = stage + L::kKElems + d0 * L::kVPitch + 2 * kp;
+    // Columns d0 + 2e and d0 + 2e + 1 of keys 2kp (low halves) and 2kp + 1 (high halves).
+    const auto put = [&](int e, uint32_t a, uint32_t b) {
+      *reinterpret_cast<uint32_t*>(vt + (2 * e) * L::kVPitch) = (a & 0xFFFFu) | (b << 16);
+      *reinterpret_cast<uint32_t*>(vt + (2 * e + 1) * L::kVPitch) = (a >> 16) | (b & 0xFFFF0000u);
+    };
+    put(0, r.v0.x, r.v1.x);
+    put(1, r.v0.y, r.v1.y);
+    put(2, r.v0.z, r.v1.z);
+    put(3, r.v0.w, r.v1.w);
+  }
+}
+
+// One 32-key block from LDS stage `kst` (keys u0 .. u0 + 31) for this wave's
+// RT row tiles: the scores of both 16-key sub-tiles, the causal mask, one
+// online-softmax update per row for the whole block, then O^T += V^T P^T.
+// The accumulator is rescaled only when some row's maximum moved (alpha is
+// exactly 1 otherwise); the test is uniform over the wave.
+template <int D, int NREP, int RT>
+__device__ __forceinline__ void pf_compute(const uint16_t* kst, int u0, int last, float qk_scale, int r16, int quad,
+                                           const int (&tr)[RT], const bf16x8_t (&qop)[RT][D / 32],
+                                           f32x4_t (&oacc)[RT][D / 16], float (&mrow)[RT], float (&lrow)[RT]) {
+  using L = PfSmem<D>;
+  constexpr int KB = D / 32, DT = D / 16, ST = kKeyBlk / 16;
+  const uint16_t* vst = kst + L::kKElems;
+  // Entry i of sub-tile st: key u0 + st*16 + quad*4 + i against row r16.
+  f32x4_t sacc[RT][ST];
+#pragma unroll
+  for (int st = 0; st < ST; ++st) {
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) sacc[rt][st] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+      const bf16x8_t kop = __builtin_bit_cast(
+          bf16x8_t, *reinterpret_cast<const uint4*>(kst + (st * 16 + r16) * L::kKPitch + kb * 32 + quad * 8));
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) sacc[rt][st] = mfma16x16x32(kop, qop[rt][kb], sacc[rt][st]);
+    }
+  }
+  bf16x4_t pop[RT][ST];
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) {
+    float x[ST][4];
+    float mloc = -INFINITY;
+#pragma unroll
+    for (int st = 0; st < ST; ++st)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int u = u0 + st * 16 + quad * 4 + i;
+        x[st][i] = (tr[rt] <= last && u <= tr[rt]) ? sacc[rt][st][i] * qk_scale : -INFINITY;
+        mloc = fmaxf(mloc, x[st][i]);
+      }
+    mloc = xor_max_from<16>(mloc);
+    const float mx = fmaxf(mrow[rt], mloc);
+    const float mu = mx == -INFINITY ? 0.f : mx;
+    const float alpha = fast_exp2(mrow[rt] - mu);
+    float psum = 0.f;
+#pragma unroll
+    for (int st = 0; st < ST; ++st) {
+      float pw[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) pw[i] = fast_exp2(x[st][i] - mu);
+      psum += (pw[0] + pw[1]) + (pw[2] + pw[3]);
+      pop[rt][st] =
+          __builtin_bit_cast(bf16x4_t, make_uint2(pack_bf16x2(pw[0], pw[1]), pack_bf16x2(pw[2], pw[3])));
+    }
+    lrow[rt] = lrow[rt] * alpha + psum;
+    mrow[rt] = mx;
+    if (__any(alpha != 1.f)) {
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) oacc[rt][dt] *= alpha;
+    }
+  }
+#pragma unroll
+  for (int st = 0; st < ST; ++st)
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+      const bf16x4_t vop = __builtin_bit_cast(
+          bf16x4_t, *reinterpret_cast<const uint2*>(vst + (dt * 16 + r16) * L::kVPitch + st * 16 + quad * 4));
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) oacc[rt][dt] = mfma16x16x16(vop, pop[rt][st], oacc[rt][dt]);
+    }
+}
+
+template <int D, int NREP, int RT>
+__global__ __launch_bounds__(kPfThreads) void prefill_attn_kernel(const PrefillArgs a, int max_blocks) {
+  using L = PfSmem<D>;
+  constexpr int KB = D / 32;              // MFMA k-blocks over head_dim
+  constexpr int DT = D / 16;              // 16-column output tiles
+  constexpr int TPT = 16 / NREP;          // prompt tokens per 16-row tile
+  constexpr int TPW = RT * TPT;           // prompt tokens per wave
+  constexpr int TPB = kPfWaves * TPW;     // prompt tokens per workgroup
+  __shared__ __attribute__((aligned(16))) uint16_t smem[L::kBytes / 2];
 
   const int Hkv = a.num_kv_heads, Hq = a.num_q_heads;
   const int NP = a.num_groups * Hkv;
   const int pair = (int)(blockIdx.x % (unsigned)NP);
-  const int tile = max_tiles - 1 - (int)(blockIdx.x / (unsigned)NP);
+  const int rb = max_blocks - 1 - (int)(blockIdx.x / (unsigned)NP);
   const int g = pair / Hkv, h = pair - g * Hkv;
   int first;
   const int P = prompt_len(a, g, &first);
-  const int t0 = tile * TPT;
-  if (t0 >= P) return;
-  const int lane = threadIdx.x, r16 = lane & 15, quad = lane >> 4;
+  const int T0 = rb * TPB;
+  if (T0 >= P) return;  // uniform over the workgroup
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6, r16 = lane & 15, quad = lane >> 4;
   const int last = P - 1;
-
-  // Row r16 of the tile: token t0 + r16 / NREP, query head h * NREP + r16 % NREP.
-  const int tr = t0 + r16 / NREP;
-  const bool row_ok = tr < P;
-  const int jr = h * NREP + r16 % NREP;
   const size_t qpitch = (size_t)Hq * D, kpitch = (size_t)Hkv * D;
-  const uint16_t* qrow = static_cast<const uint16_t*>(a.q) + (size_t)(first + min(tr, last)) * qpitch + (size_t)jr * D;
   const uint16_t* kbase = static_cast<const uint16_t*>(a.k) + (size_t)first * kpitch + (size_t)h * D;
   const uint16_t* vbase = static_cast<const uint16_t*>(a.v) + (size_t)first * kpitch + (size_t)h * D;
-  uint16_t* qt_lane = qt + r16 * QSTRIDE + quad * 8;
+
+  // Row r16 of row tile rt: token T0 + wave * TPW + rt * TPT + r16 / NREP,
+  // query head h * NREP + r16 % NREP. Q is the B operand of S^T = K Q^T.
+  const int jr = h * NREP + r16 % NREP;
+  int tr[RT];
+  bf16x8_t qop[RT][KB];
 #pragma unroll
-  for (int kb = 0; kb < KB; ++kb) {
-    uint4 w = make_uint4(0, 0, 0, 0);
-    if (row_ok) w = *reinterpret_cast<const uint4*>(qrow + kb * 32 + quad * 8);
-    *reinterpret_cast<uint4*>(qt_lane + kb * 32) = w;
+  for (int rt = 0; rt < RT; ++rt) {
+    tr[rt] = T0 + wave * TPW + rt * TPT + r16 / NREP;
+    const uint16_t* qrow = static_cast<const uint16_t*>(a.q) + (size_t)(first + min(tr[rt], last)) * qpitch +
+                           (size_t)jr * D + quad * 8;
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) qop[rt][kb] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(qrow + kb * 32));
   }
 
-  const int tlast = min(t0 + TPT, P) - 1;  // the tile's last token bounds its keys
-  const int nblk = tlast / kPage + 1;
-  float mrow = -INFINITY, lrow = 0.f;
-  f32x4_t oacc[DT];
+  const int tlast = min(T0 + TPB, P) - 1;  // the workgroup's last token bounds its keys
+  const int nblk = tlast / kKeyBlk + 1;
+  float mrow[RT], lrow[RT];
+  f32x4_t oacc[RT][DT];
 #pragma unroll
-  for (int dt = 0; dt < DT; ++dt) oacc[dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  for (int rt = 0; rt < RT; ++rt) {
+    mrow[rt] = -INFINITY;
+    lrow[rt] = 0.f;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) oacc[rt][dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  }
 
-  KeyBlock<D> kv;
-  load_block_k<D>(kbase, kpitch, 0, last, lane, kv);
-  load_block_v<D>(vbase, kpitch, 0, last, lane, kv);
+  // The next block's loads are issued before this block's compute and
+  // written to the other LDS buffer after it (past the last block they read
+  // clamped rows and are never used).
+  PfBlock nx;
+  pf_load<D>(kbase, vbase, kpitch, 0, last, t, nx);
+  pf_store<D>(smem, t, nx);
+  __syncthreads();
   for (int blk = 0; blk < nblk; ++blk) {
-    const int u0 = blk * kPage;
-    const int un = blk + 1 < nblk ? u0 + kPage : u0;  // the next block (this one again after the last)
+    pf_load<D>(kbase, vbase, kpitch, (blk + 1) * kKeyBlk, last, t, nx);
+    pf_compute<D, NREP, RT>(smem + (blk & 1) * L::kStage, blk * kKeyBlk, last, a.qk_scale, r16, quad, tr, qop,
+                            oacc, mrow, lrow);
+    pf_store<D>(smem + ((blk + 1) & 1) * L::kStage, t, nx);
+    __syncthreads();  // the next block is staged; this block's buffer may be overwritten next
+  }
 
-    // Stage this block's V (rows past the prompt as zeros), then request the next.
-    __syncthreads();  // the previous block's LDS reads (and the query tile writes) are complete
 #pragma unroll
-    for (int i = 0; i < kPage * D * 2 / 1024; ++i) {
-      const int e0 = i * 512 + lane * 8;
-      const int tok = e0 / D, col = e0 % D;
-      const uint4 w = u0 + tok <= last ? kv.v[i] : make_uint4(0, 0, 0, 0);
-      uint2* dst = reinterpret_cast<uint2*>(vt + tok * STRIDE + col);
-      dst[0] = make_uint2(w.x, w.y);
-      dst[1] = make_uint2(w.z, w.w);
-    }
-    __builtin_amdgcn_sched_barrier(0);
-    load_block_v<D>(vbase, kpitch, un, last, lane, kv);
-
-    // Entry i of this lane: key u0 + quad*4 + i against tile row r16.
-    f32x4_t sacc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int kb = 0; kb < KB; ++kb) {
-      const bf16x8_t qop = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(qt_lane + kb * 32));
-      sacc = mfma16x16x32(__builtin_bit_cast(bf16x8_t, kv.k[kb]), qop, sacc);
-    }
-    __builtin_amdgcn_sched_barrier(0);
-    load_block_k<D>(kbase, kpitch, un, last, lane, kv);
-
-    float x[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int u = u0 + quad * 4 + i;
-      x[i] = (row_ok && u <= tr) ? sacc[i] * a.qk_scale : -INFINITY;
-    }
-    float mloc = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
-    mloc = xor_max_from<16>(mloc);
-    const float mx = fmaxf(mrow, mloc);
-    const float mu = mx == -INFINITY ? 0.f : mx;
-    const float alpha = fast_exp2(mrow - mu);
-    float pw[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) pw[i] = fast_exp2(x[i] - mu);
-    lrow = lrow * alpha + ((pw[0] + pw[1]) + (pw[2] + pw[3]));
-    mrow = mx;
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt) oacc[dt] *= alpha;
-    const bf16x4_t pop =
-        __builtin_bit_cast(bf16x4_t, make_uint2(pack_bf16x2(pw[0], pw[1]), pack_bf16x2(pw[2], pw[3])));
-
-    __syncthreads();  // the staged V is visible
+  for (int rt = 0; rt < RT; ++rt) {
+    const float lt = xor_sum_from<16>(lrow[rt]);
+    if (tr[rt] > last) continue;
+    const float inv = 1.f / lt;
+    uint16_t* orow = static_cast<uint16_t*>(a.out) + (size_t)(first + tr[rt]) * qpitch + (size_t)jr * D + quad * 4;
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
-      const uint16_t* col = vt + (quad * 4) * STRIDE + dt * 16 + r16;
-      const uint32_t w0 = (uint32_t)col[0] | ((uint32_t)col[STRIDE] << 16);
-      const uint32_t w1 = (uint32_t)col[2 * STRIDE] | ((uint32_t)col[3 * STRIDE] << 16);
-      oacc[dt] = mfma16x16x16(__builtin_bit_cast(bf16x4_t, make_uint2(w0, w1)), pop, oacc[dt]);
-      __builtin_amdgcn_sched_barrier(0);
+      const f32x4_t v = oacc[rt][dt] * inv;
+      *reinterpret_cast<uint2*>(orow + dt * 16) = make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
     }
+    if (a.lse != nullptr && quad == 0) a.lse[(size_t)(first + tr[rt]) * Hq + jr] = (mrow[rt] + fast_log2(lt)) * kLn2;
   }
+}
 
-  const float lt = xor_sum_from<16>(lrow);
-  if (!row_ok) return;
-  const float inv = 1.f / lt;
-  uint16_t* orow = static_cast<uint16_t*>(a.out) + (size_t)(first + tr) * qpitch + (size_t)jr * D + quad * 4;
-#pragma unroll
-  for (int dt = 0; dt < DT; ++dt) {
-    const f32x4_t v = oacc[dt] * inv;
-    *reinterpret_cast<uint2*>(orow + dt * 16) = make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
-  }
-  if (a.lse != nullptr && quad == 0) a.lse[(size_t)(first + tr) * Hq + jr] = (mrow + fast_log2(lt)) * kLn2;
+// Row tiles per wave: two on long prompts (each K/V operand read from LDS
+// serves two MFMAs), one otherwise (more workgroups).
+template <int D, int NREP>
+hipError_t attn_launch(const PrefillArgs& a, hipStream_t st) {
+  const long long NP = (long long)a.num_groups * a.num_kv_heads;
+  const int max_tokens = a.max_prefix_pages * kPage;
+  const int rt = max_tokens >= 1024 ? 2 : 1;
+  const int tpb = kPfWaves * rt * (16 / NREP);
+  const int max_blocks = cdiv(max_tokens, tpb);
+  const long long blocks = NP * max_blocks;
+  if (blocks <= 0) return hipSuccess;
+  const dim3 grid((unsigned)blocks), block(kPfThreads);
+  if (rt == 2) prefill_attn_kernel<D, NREP, 2><<<grid, block, 0, st>>>(a, max_blocks);
+  else prefill_attn_kernel<D, NREP, 1><<<grid, block, 0, st>>>(a, max_blocks);
+  return hipGetLastError();
 }
 
 template <int D>
 hipError_t attn_by_nrep(const PrefillArgs& a, int n_rep, hipStream_t st) {
-  const long long NP = (long long)a.num_groups * a.num_kv_heads;
-  const int max_tiles = cdiv(a.max_prefix_pages * kPage, 16 / n_rep);
-  const long long blocks = NP * max_tiles;
-  if (blocks <= 0) return hipSuccess;
-  const dim3 grid((unsigned)blocks), block(64);
   switch (n_rep) {
-    case 1: prefill_attn_kernel<D, 1><<<grid, block, 0, st>>>(a, max_tiles); break;
-    case 2: prefill_attn_kernel<D, 2><<<grid, block, 0, st>>>(a, max_tiles); break;
-    case 4: prefill_attn_kernel<D, 4><<<grid, block, 0, st>>>(a, max_tiles); break;
-    case 8: prefill_attn_kernel<D, 8><<<grid, block, 0, st>>>(a, max_tiles); break;
+    case 1: return attn_launch<D, 1>(a, st);
+    case 2: return attn_launch<D, 2>(a, st);
+    case 4: return attn_launch<D, 4>(a, st);
+    case 8: return attn_launch<D, 8>(a, st);
     default: return hipErrorInvalidValue;
   }
-  return hipGetLastError();
 }
 
 }  // namespace
