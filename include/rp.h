@@ -216,7 +216,7 @@ rp_status rp_prefill_kv_write(const rp_paged_kv* kv, const rp_prefill_layout* la
  *   out[t][j] = sum_u exp(s_u - lse) v_u.
  * Reads the bf16 projections q, k, v (not the pool; the pool only supplies
  * Hkv and head_dim). out: bf16 [T][Hq][head_dim], 16-byte aligned; lse: fp32
- * [T][Hq], natural log, may be NULL. */
+ * [T][Hq], natural log, may be NULL. softmax_scale must be finite and > 0. */
 rp_status rp_prefill_attn(const rp_paged_kv* kv, const rp_prefill_layout* layout,
                           const void* q, const void* k, const void* v, float softmax_scale,
                           void* out, float* lse, hipStream_t stream);

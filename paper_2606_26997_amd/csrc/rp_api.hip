@@ -482,6 +482,8 @@ rp_status rp_prefill_attn(const rp_paged_kv* kv, const rp_prefill_layout* l, con
   int n_rep = 0;
   rp_status st = prefill_args(kv, l, &a, &n_rep);
   if (st != RP_OK) return st;
+  if (!(softmax_scale > 0.f) || !std::isfinite(softmax_scale))
+    return fail(RP_ERR_INVALID_ARG, "softmax_scale must be finite and > 0");
   if (l->num_groups == 0 || l->num_tokens == 0) return RP_OK;
   if (q == nullptr || k == nullptr || v == nullptr || !aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16))
     return fail(RP_ERR_INVALID_ARG, "q/k/v must be non-NULL and 16-byte aligned");

@@ -194,8 +194,9 @@ __device__ inline void pf_store(uint16_t* stage, int t, const PfBlock& r) {
 // RT row tiles: the scores of both 16-key sub-tiles, the causal mask, one
 // online-softmax update per row for the whole block, then O^T += V^T P^T.
 // The accumulator is rescaled only when some row's maximum moved (alpha is
-// exactly 1 otherwise); the test is uniform over the wave.
-template <int D, int NREP, int RT>
+// exactly 1 otherwise); the test is uniform over the wave. MASK = false for
+// blocks that lie wholly at or below the diagonal of every row of the wave.
+template <int D, int NREP, int RT, bool MASK>
 __device__ __forceinline__ void pf_compute(const uint16_t* kst, int u0, int last, float qk_scale, int r16, int quad,
                                            const int (&tr)[RT], const bf16x8_t (&qop)[RT][D / 32],
                                            f32x4_t (&oacc)[RT][D / 16], float (&mrow)[RT], float (&lrow)[RT]) {
@@ -219,17 +220,23 @@ __device__ __forceinline__ void pf_compute(const uint16_t* kst, int u0, int last
   bf16x4_t pop[RT][ST];
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt) {
+    // Raw scores (masked to -inf); the scale is applied inside the exponent,
+    // max(s * c) = max(s) * c for c > 0.
     float x[ST][4];
     float mloc = -INFINITY;
 #pragma unroll
     for (int st = 0; st < ST; ++st)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int u = u0 + st * 16 + quad * 4 + i;
-        x[st][i] = (tr[rt] <= last && u <= tr[rt]) ? sacc[rt][st][i] * qk_scale : -INFINITY;
+        if constexpr (MASK) {
+          const int u = u0 + st * 16 + quad * 4 + i;
+          x[st][i] = (tr[rt] <= last && u <= tr[rt]) ? sacc[rt][st][i] : -INFINITY;
+        } else {
+          x[st][i] = sacc[rt][st][i];
+        }
         mloc = fmaxf(mloc, x[st][i]);
       }
-    mloc = xor_max_from<16>(mloc);
+    mloc = xor_max_from<16>(mloc) * qk_scale;
     const float mx = fmaxf(mrow[rt], mloc);
     const float mu = mx == -INFINITY ? 0.f : mx;
     const float alpha = fast_exp2(mrow[rt] - mu);
@@ -238,7 +245,7 @@ __device__ __forceinline__ void pf_compute(const uint16_t* kst, int u0, int last
     for (int st = 0; st < ST; ++st) {
       float pw[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) pw[i] = fast_exp2(x[st][i] - mu);
+      for (int i = 0; i < 4; ++i) pw[i] = fast_exp2(fmaf(x[st][i], qk_scale, -mu));
       psum += (pw[0] + pw[1]) + (pw[2] + pw[3]);
       pop[rt][st] =
           __builtin_bit_cast(bf16x4_t, make_uint2(pack_bf16x2(pw[0], pw[1]), pack_bf16x2(pw[2], pw[3])));
@@ -301,6 +308,7 @@ __global__ __launch_bounds__(kPfThreads) void prefill_attn_kernel(const PrefillA
   }
 
   const int tlast = min(T0 + TPB, P) - 1;  // the workgroup's last token bounds its keys
+  const int w_first = T0 + wave * TPW, w_last = w_first + TPW - 1;  // this wave's tokens
   const int nblk = tlast / kKeyBlk + 1;
   float mrow[RT], lrow[RT];
   f32x4_t oacc[RT][DT];
@@ -321,8 +329,13 @@ __global__ __launch_bounds__(kPfThreads) void prefill_attn_kernel(const PrefillA
   __syncthreads();
   for (int blk = 0; blk < nblk; ++blk) {
     pf_load<D>(kbase, vbase, kpitch, (blk + 1) * kKeyBlk, last, t, nx);
-    pf_compute<D, NREP, RT>(smem + (blk & 1) * L::kStage, blk * kKeyBlk, last, a.qk_scale, r16, quad, tr, qop,
-                            oacc, mrow, lrow);
+    // Blocks wholly below the diagonal for every (valid) row of the wave skip the mask.
+    if ((blk + 1) * kKeyBlk - 1 <= w_first && w_last <= last)
+      pf_compute<D, NREP, RT, false>(smem + (blk & 1) * L::kStage, blk * kKeyBlk, last, a.qk_scale, r16, quad, tr,
+                                     qop, oacc, mrow, lrow);
+    else
+      pf_compute<D, NREP, RT, true>(smem + (blk & 1) * L::kStage, blk * kKeyBlk, last, a.qk_scale, r16, quad, tr,
+                                    qop, oacc, mrow, lrow);
     pf_store<D>(smem + ((blk + 1) & 1) * L::kStage, t, nx);
     __syncthreads();  // the next block is staged; this block's buffer may be overwritten next
   }

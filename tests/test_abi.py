@@ -199,6 +199,9 @@ def test_prefill_pointer_checks():
     assert st == rp.RP_ERR_INVALID_ARG and "out" in rp.last_error()
     st = lib.rp_prefill_attn(ctypes.byref(kv), ctypes.byref(lay), A, A, A, ctypes.c_float(0.1), A, A + 2, None)
     assert st == rp.RP_ERR_INVALID_ARG and "lse" in rp.last_error()
+    for bad in (0.0, -0.1, float("inf"), float("nan")):
+        st = lib.rp_prefill_attn(ctypes.byref(kv), ctypes.byref(lay), A, A, A, ctypes.c_float(bad), A, None, None)
+        assert st == rp.RP_ERR_INVALID_ARG and "softmax_scale" in rp.last_error()
     # Nothing to do: returns before touching any pointer.
     assert lib.rp_prefill_attn(ctypes.byref(kv), ctypes.byref(_prefill_layout(num_tokens=0)), None, None, None,
                                ctypes.c_float(0.1), None, None, None) == rp.RP_OK
