@@ -355,13 +355,14 @@ __global__ __launch_bounds__(kPfThreads) void prefill_attn_kernel(const PrefillA
   }
 }
 
-// Row tiles per wave: two on long prompts (each K/V operand read from LDS
-// serves two MFMAs), one otherwise (more workgroups).
+// Row tiles per wave: two when prompts average 384 tokens or more (each K/V
+// operand read from LDS serves two MFMAs), one otherwise (twice the
+// workgroups, which balances ragged short prompts better; measured).
 template <int D, int NREP>
 hipError_t attn_launch(const PrefillArgs& a, hipStream_t st) {
   const long long NP = (long long)a.num_groups * a.num_kv_heads;
   const int max_tokens = a.max_prefix_pages * kPage;
-  const int rt = max_tokens >= 1024 ? 2 : 1;
+  const int rt = (long long)a.num_tokens >= 384ll * a.num_groups ? 2 : 1;
   const int tpb = kPfWaves * rt * (16 / NREP);
   const int max_blocks = cdiv(max_tokens, tpb);
   const long long blocks = NP * max_blocks;

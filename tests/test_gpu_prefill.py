@@ -1,7 +1,9 @@
 """GPU parity of the shared-prefix prefill through the C ABI against the fp64 oracle.
 
 The page write is compared byte for byte (bf16 copies and fp8 codes with their
-scales); causal attention element by element at the decode path's tolerances.
+scales); causal attention element by element at the decode path's tolerances,
+the max-abs bound widened by half a bf16 ulp of each exact value (the output
+format's rounding).
 An end-to-end case decodes each prompt's last token over the pages the prefill
 wrote and checks it against the prefill's own last row.
 """
@@ -52,8 +54,13 @@ def _check_attn(b, w, label, rows=None):
     if rows is not None:
         out, lse, ref_out, ref_lse = out[rows], lse[rows], ref_out[rows], ref_lse[rows]
     tol = TOL["bf16"]
-    err = np.abs(out - ref_out)
-    rel = np.sqrt((err ** 2).sum() / max((ref_out ** 2).sum(), 1e-300))
+    # The output is bf16: the bound covers the computation plus the format's
+    # own rounding, half a bf16 ulp of the exact value. Early prompt tokens
+    # attend few keys and reach |out| ~ 4, where that half-ulp alone is 0.0078.
+    half_ulp = np.ldexp(1.0, np.frexp(np.abs(ref_out))[1] - 9)
+    diff = np.abs(out - ref_out)
+    err = np.maximum(diff - half_ulp, 0.0)
+    rel = np.sqrt((diff ** 2).sum() / max((ref_out ** 2).sum(), 1e-300))
     dl = np.abs(lse - ref_lse)
     msg = f"{label}: max_abs={err.max():.3e} rel_l2={rel:.3e} max_dlse={dl.max():.3e}"
     assert err.max() <= tol["max_abs"], msg
@@ -70,6 +77,10 @@ CASES = [
     ("nrep8", [25, 9], 8, 1, 128, "bf16"),
     ("fp8-pages", [1, 16, 17, 100], 16, 8, 128, "fp8"),
     ("fp8-d64", [48, 2], 4, 2, 64, "fp8"),
+    # Prompts averaging 384+ tokens take two 16-row tiles per wave.
+    ("long-two-tiles-d128", [400, 700, 513, 385], 16, 8, 128, "bf16"),
+    ("long-two-tiles-d64-nrep4", [450, 390, 1], 8, 2, 64, "bf16"),
+    ("long-two-tiles-nrep8", [600, 255], 8, 1, 128, "bf16"),
 ]
 
 
