@@ -197,6 +197,19 @@ __device__ inline float xor_sum_from(float x) {
   return x;
 }
 
+// Max over lanes l, l^16, l^32, l^48 (the four quads of an MFMA tile column)
+// with gfx950's row-swap instructions, which stay in the VALU: swapping the
+// halves (rows) of two copies of x puts x[l] and x[l^32] (x[l^16]) into the
+// two results of every lane.
+__device__ inline float max_xor16_32(float x) {
+  const uint32_t u = __float_as_uint(x);
+  const auto a = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const uint32_t v = __float_as_uint(x);
+  const auto b = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+
 // MFMA tiles used by the group-prefix and prefill paths (fp32 accumulate):
 //   16x16x32 bf16: lane (r, q) supplies A[r][8q..8q+7] and B[8q..8q+7][r];
 //   16x16x16 bf16: lane (r, q) supplies A[r][4q..4q+3] and B[4q..4q+3][r];

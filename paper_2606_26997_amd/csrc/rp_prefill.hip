@@ -113,10 +113,11 @@ __global__ __launch_bounds__(64) void prefill_kv_write_kernel(const PrefillArgs 
 // from the projections and written into the other buffer; one barrier per
 // block. Per block and row tile: S^T = K Q^T on mfma 16x16x32 (Q stays in
 // registers), a causal mask, one online-softmax update per row, and
-// O^T += V^T P^T on mfma 16x16x16.
+// O^T += V^T P^T, also on mfma 16x16x32 (all 32 keys per instruction).
 constexpr int kPfWaves = 4;
 constexpr int kPfThreads = 64 * kPfWaves;
 constexpr int kKeyBlk = 32;
+constexpr float kLazyMax = 8.0f;  // headroom of the running softmax maximum, log2 units
 
 template <int D>
 struct PfSmem {
@@ -193,8 +194,9 @@ __device__ inline void pf_store(uint16_t* stage, int t, const PfBlock& r) {
 // One 32-key block from LDS stage `kst` (keys u0 .. u0 + 31) for this wave's
 // RT row tiles: the scores of both 16-key sub-tiles, the causal mask, one
 // online-softmax update per row for the whole block, then O^T += V^T P^T.
-// The accumulator is rescaled only when some row's maximum moved (alpha is
-// exactly 1 otherwise); the test is uniform over the wave. MASK = false for
+// A row's running maximum moves only when a block exceeds it by more than
+// kLazyMax; the accumulator is rescaled only when some row's maximum moved
+// (alpha is exactly 1 otherwise), a test uniform over the wave. MASK = false for
 // blocks that lie wholly at or below the diagonal of every row of the wave.
 template <int D, int NREP, int RT, bool MASK>
 __device__ __forceinline__ void pf_compute(const uint16_t* kst, int u0, int last, float qk_scale, int r16, int quad,
@@ -236,10 +238,14 @@ __device__ __forceinline__ void pf_compute(const uint16_t* kst, int u0, int last
         }
         mloc = fmaxf(mloc, x[st][i]);
       }
-    mloc = xor_max_from<16>(mloc) * qk_scale;
-    const float mx = fmaxf(mrow[rt], mloc);
-    const float mu = mx == -INFINITY ? 0.f : mx;
+    mloc = max_xor16_32(mloc) * qk_scale;
+    // The running maximum moves only when this block exceeds it by more than
+    // kLazyMax (log2 units): the probabilities then stay below 2^kLazyMax,
+    // and most blocks leave the accumulator unscaled (alpha = exp2(0) = 1).
+    const float mnew = mloc > mrow[rt] + kLazyMax ? mloc : mrow[rt];
+    const float mu = mnew == -INFINITY ? 0.f : mnew;
     const float alpha = fast_exp2(mrow[rt] - mu);
+    mrow[rt] = mnew;
     float psum = 0.f;
 #pragma unroll
     for (int st = 0; st < ST; ++st) {
@@ -251,21 +257,29 @@ __device__ __forceinline__ void pf_compute(const uint16_t* kst, int u0, int last
           __builtin_bit_cast(bf16x4_t, make_uint2(pack_bf16x2(pw[0], pw[1]), pack_bf16x2(pw[2], pw[3])));
     }
     lrow[rt] = lrow[rt] * alpha + psum;
-    mrow[rt] = mx;
     if (__any(alpha != 1.f)) {
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) oacc[rt][dt] *= alpha;
     }
   }
+  // O^T += V^T P^T over all 32 keys in one mfma 16x16x32 per 16 output
+  // columns: lane (r16, quad) supplies contraction slots 8 quad .. 8 quad + 7,
+  // taken as keys quad*4 .. quad*4 + 3 and 16 + quad*4 .. 16 + quad*4 + 3 in
+  // both operands (any key order serves, as long as V^T and P^T share it).
+  static_assert(ST == 2, "two 16-key sub-tiles per block");
+  bf16x8_t pop8[RT];
 #pragma unroll
-  for (int st = 0; st < ST; ++st)
+  for (int rt = 0; rt < RT; ++rt)
+    pop8[rt] = __builtin_shufflevector(pop[rt][0], pop[rt][1], 0, 1, 2, 3, 4, 5, 6, 7);
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) {
-      const bf16x4_t vop = __builtin_bit_cast(
-          bf16x4_t, *reinterpret_cast<const uint2*>(vst + (dt * 16 + r16) * L::kVPitch + st * 16 + quad * 4));
+  for (int dt = 0; dt < DT; ++dt) {
+    const uint16_t* vrow = vst + (dt * 16 + r16) * L::kVPitch + quad * 4;
+    const bf16x4_t v0 = __builtin_bit_cast(bf16x4_t, *reinterpret_cast<const uint2*>(vrow));
+    const bf16x4_t v1 = __builtin_bit_cast(bf16x4_t, *reinterpret_cast<const uint2*>(vrow + 16));
+    const bf16x8_t vop = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
 #pragma unroll
-      for (int rt = 0; rt < RT; ++rt) oacc[rt][dt] = mfma16x16x16(vop, pop[rt][st], oacc[rt][dt]);
-    }
+    for (int rt = 0; rt < RT; ++rt) oacc[rt][dt] = mfma16x16x32(vop, pop8[rt], oacc[rt][dt]);
+  }
 }
 
 template <int D, int NREP, int RT>
