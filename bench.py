@@ -264,6 +264,37 @@ def prefill_bench(args):
     print(json.dumps(line), flush=True)
 
 
+def _model_step_ms(b, steps, layers=None, min_bytes=2e9):
+    """One decode step of a model: one plan (the lengths are shared by all layers), then per layer
+    q/k prep, partial attention and combine. Layers cycle through enough copies of the K/V pool
+    (same page layout) that the K/V read per step exceeds `min_bytes`, so that, unlike one layer
+    repeated, they come from HBM rather than the 256 MB last-level cache."""
+    import torch
+    import paper_2606_26997_amd as rp
+    layers = QWEN3_LAYERS if layers is None else layers
+    pool_bytes = 2 * b.k_pages.numel() * b.k_pages.element_size()
+    copies = int(min(layers, max(1, -(-min_bytes // pool_bytes))))
+    pools = [(b.k_pages, b.v_pages)] + [(b.k_pages.clone(), b.v_pages.clone()) for _ in range(copies - 1)]
+    kvs = [rp.paged_kv(kp, vp) for kp, vp in pools]
+
+    def model_step():
+        rp.plan(kvs[0], b.attn_layout, b.workspace)
+        for l in range(layers):
+            kv = kvs[l % copies]
+            rp.decode_qk_prep(kv, b.append_layout, b.q_in, b.k_in, b.v_in, b.q_norm_w, b.k_norm_w, b.q, None)
+            rp.attn_parts(kv, b.attn_layout, b.q, b.softmax_scale, b.workspace)
+            rp.combine_parts(kv, b.attn_layout, b.out, b.lse, b.workspace)
+
+    for _ in range(2):
+        model_step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        model_step()
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) / steps * 1e3, copies
+
+
 FGD_GROUPS, FGD_LIVE, FGD_PREFIX, FGD_RESP_MAX = 2, 8, 512, 6016
 
 
@@ -324,6 +355,10 @@ def fgd_bench(args):
     parts_us = per["parts"]
     achieved = bm["parts_kernel"] / (parts_us * 1e-6) / 1e9
 
+    # A whole model step (see _model_step_ms): K/V from HBM, one plan per step.
+    model_ms, copies = _model_step_ms(b, max(args.steps // 10, 5))
+    layer_bytes = total
+
     # The prep kernel alone on a large batch (4096 sequences, one response page
     # each): q read and written, k and v read and appended.
     S2 = 4096
@@ -354,6 +389,10 @@ def fgd_bench(args):
                    "prefix_tokens": bm["prefix_tokens"], "resp_tokens": bm["resp_tokens"], "seed": seed},
         "GBps": round(total / (ms * 1e-3) / 1e9, 1), "algorithmic_bytes_per_step": int(total),
         "kernel_us": {k: round(v, 2) for k, v in per.items()},
+        "model_step": {"layers": QWEN3_LAYERS, "kv_pool_copies": copies, "ms": round(model_ms, 4),
+                       "per_layer_us": round(model_ms * 1e3 / QWEN3_LAYERS, 2),
+                       "seq_steps_per_s": round(S / (model_ms * 1e-3), 1),
+                       "GBps": round(QWEN3_LAYERS * layer_bytes / (model_ms * 1e-3) / 1e9, 1)},
         "prep_4096_seqs": {"us": round(prep_us, 2), "bytes": prep_bytes,
                            "GBps": round(prep_bytes / (prep_us * 1e-6) / 1e9, 1)},
         "roofline": {"kernel": "attn_parts_kernel", "bound": "hbm", "achieved": round(achieved, 1),
@@ -372,9 +411,10 @@ PAPER_TRAIN_R96 = 587.4                                    # trainer compute, LS
 PAPER_ROLLOUT_R96 = 525.0                                  # mid-range of Slime's first dispatch at R = 96 (509-543 s)
 
 
-def _measure_decode_layer(args, rng):
-    """Per-layer decode-step time (q/k prep + plan + attention + combine) at several batch shapes,
-    fitted as a + b * sequences + c * context tokens (context counted per sequence, prompt included)."""
+def _measure_decode_step(args, rng):
+    """Attention part of a whole-model decode step (one plan, then per layer q/k prep, partial
+    attention and combine; K/V from HBM) at several batch shapes, fitted as
+    a + b * sequences + c * context tokens (context counted per sequence, prompt included)."""
     import numpy as np
     import torch
     import paper_2606_26997_amd as rp
@@ -388,18 +428,13 @@ def _measure_decode_layer(args, rng):
         x = make_qkprep_inputs(num_seqs=S, num_q_heads=16, num_kv_heads=8, head_dim=128, seed=S)
         b = rp.DeviceBatch.from_workload(wl, device="cuda:0")
         b.set_projections(x.q_in, x.k_in, x.v_in, x.q_norm_w, x.k_norm_w)
-        for _ in range(10):
-            b.decode_step()
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        for _ in range(50):
-            b.decode_step()
-        torch.cuda.synchronize()
-        times.append((time.perf_counter() - t0) / 50)
+        ms, _ = _model_step_ms(b, 5)
+        times.append(ms * 1e-3)
         rows.append([1.0, S, float(512 * S + resp.sum() + S)])
         del b
+        torch.cuda.empty_cache()
     coef, *_ = np.linalg.lstsq(np.array(rows), np.array(times), rcond=None)
-    return [float(c) for c in coef], [dict(seqs=int(r[1]), ctx_tokens=int(r[2]), us=round(t * 1e6, 2))
+    return [float(c) for c in coef], [dict(seqs=int(r[1]), ctx_tokens=int(r[2]), ms=round(t * 1e3, 4))
                                       for r, t in zip(rows, times)]
 
 
@@ -448,12 +483,12 @@ def sim_bench(args):
 
     torch.cuda.set_device(0)
     rng = np.random.default_rng(77 if args.seed is None else args.seed)
-    (a, b, c), points = _measure_decode_layer(args, rng)
+    (a, b, c), points = _measure_decode_step(args, rng)
     pre_tok = _measure_prefill_token()
     t_w = _measure_weight_read()
     per_tok_gemm = 2 * QWEN3_PARAMS / GEMM_FLOPS
-    cost = dict(step_base=QWEN3_LAYERS * max(a, 0.0) + t_w, step_per_seq=QWEN3_LAYERS * max(b, 0.0) + per_tok_gemm,
-                step_per_ctx_token=QWEN3_LAYERS * max(c, 0.0), prefill_per_token=QWEN3_LAYERS * pre_tok + per_tok_gemm)
+    cost = dict(step_base=max(a, 0.0) + t_w, step_per_seq=max(b, 0.0) + per_tok_gemm,
+                step_per_ctx_token=max(c, 0.0), prefill_per_token=QWEN3_LAYERS * pre_tok + per_tok_gemm)
     K, U, Fw, P_MAX, CAP = 8, 2, 2, 1024, 8192
 
     # Concurrency from the KV memory left after the weights, at the average context of a request
@@ -527,9 +562,9 @@ def sim_bench(args):
                                "responses lognormal (median 3000; group sigma 0.5, sample sigma 0.3; cap 8192)",
                    "max_running_mi355x": cap_mi355x, "max_running_2xA100": cap_a100},
         "cost_model": {k: float(f"{v:.6g}") for k, v in cost.items()},
-        "measured": {"decode_layer_fit_us": {"base": round(a * 1e6, 3), "per_seq": round(b * 1e6, 5),
-                                             "per_ctx_token": round(c * 1e6, 8)},
-                     "decode_layer_points": points, "prefill_layer_us_per_token": round(pre_tok * 1e6, 5),
+        "measured": {"decode_step_fit_us": {"base": round(a * 1e6, 3), "per_seq": round(b * 1e6, 5),
+                                            "per_ctx_token": round(c * 1e6, 8)},
+                     "decode_step_points": points, "prefill_layer_us_per_token": round(pre_tok * 1e6, 5),
                      "weight_read_ms": round(t_w * 1e3, 4)},
         "assumed": {"gemm_flops": GEMM_FLOPS, "materialise_s_per_group": 1.0,
                     "trainer_s_per_token_from_paper_R96": PAPER_TRAIN_R96},
