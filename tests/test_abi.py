@@ -91,6 +91,13 @@ def test_invalid_arguments_rejected(kv_kw, lay_kw, status, needle):
     assert needle in rp.last_error()
 
 
+def test_planner_group_limit():
+    # 4096 groups is the largest plan; one more is refused before any launch.
+    assert _ws_size(_kv(), _layout(num_groups=4096))[0] == rp.RP_OK
+    st, _ = _ws_size(_kv(), _layout(num_groups=4097))
+    assert st == rp.RP_ERR_UNSUPPORTED and "limit" in rp.last_error()
+
+
 def test_null_structs_rejected():
     assert _ws_size(None, _layout())[0] == rp.RP_ERR_INVALID_ARG
     assert _ws_size(_kv(), None)[0] == rp.RP_ERR_INVALID_ARG

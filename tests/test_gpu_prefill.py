@@ -106,6 +106,16 @@ def test_qwen_layer_prompts_full():
     _check_attn(b, w, "qwen-prompts")
 
 
+def test_long_prompts():
+    # Largest prompts of the tests: a 4096-token prompt (256 prefix pages) and a
+    # ragged 2200-token one; 128 key blocks for the last rows.
+    _say("prefill 4096 + 2200 tokens")
+    w = make_prefill_workload(num_q_heads=16, num_kv_heads=8, head_dim=128, prefix_lens=[4096, 2200], seed=4096)
+    b = _run(w)
+    _check_pages(b, w, "long-prompts")
+    _check_attn(b, w, "long-prompts")
+
+
 def test_decode_over_prefilled_pages_matches_last_prompt_row():
     import paper_2606_26997_amd as rp
     _say("prefill then decode the last prompt tokens")
