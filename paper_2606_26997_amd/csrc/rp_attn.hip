@@ -102,11 +102,6 @@ __device__ inline void unpack_bf16x8(const uint4& w, float* f) {
   f[6] = bf16_lo(w.w); f[7] = bf16_hi(w.w);
 }
 
-// Two floats known to be exact in bf16 -> packed bf16 pair (truncation is exact).
-__device__ inline uint32_t pack_exact_bf16x2(float lo, float hi) {
-  return (__float_as_uint(lo) >> 16) | (__float_as_uint(hi) & 0xFFFF0000u);
-}
-
 // 4 e4m3 codes -> 4 exact floats (gfx950 converts OCP e4m3fn in hardware).
 __device__ inline void e4m3x4_to_f32(uint32_t w, float* f) {
   const auto lo = __builtin_amdgcn_cvt_pk_f32_fp8((int)w, false);
@@ -122,13 +117,15 @@ __device__ inline void unpack_e4m3x16(const uint4& w, float* f) {
   e4m3x4_to_f32(w.z, f + 8);
   e4m3x4_to_f32(w.w, f + 12);
 }
-// 8 e4m3 codes -> 8 bf16 values (exact: every e4m3 value is a bf16 value).
+// 8 e4m3 codes -> 8 bf16 values (exact: every e4m3 value is a bf16 value), by
+// gfx950's scaled conversion with scale 1: two codes per instruction.
+template <bool HIGH>
+__device__ inline uint32_t e4m3x2_to_bf16x2(uint32_t w) {
+  return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.0f, HIGH));
+}
 __device__ inline uint4 e4m3x8_to_bf16x8(uint32_t w0, uint32_t w1) {
-  float f[8];
-  e4m3x4_to_f32(w0, f);
-  e4m3x4_to_f32(w1, f + 4);
-  return make_uint4(pack_exact_bf16x2(f[0], f[1]), pack_exact_bf16x2(f[2], f[3]),
-                    pack_exact_bf16x2(f[4], f[5]), pack_exact_bf16x2(f[6], f[7]));
+  return make_uint4(e4m3x2_to_bf16x2<false>(w0), e4m3x2_to_bf16x2<true>(w0), e4m3x2_to_bf16x2<false>(w1),
+                    e4m3x2_to_bf16x2<true>(w1));
 }
 
 template <int D, bool FP8>
@@ -502,10 +499,13 @@ __device__ void resp_unit(const AttnArgs& a, int item, int h, char* smem) {
 
 #pragma unroll
     for (int r = 0; r < NREP; ++r) {
-      float mx = mrun[r];
+      float mx = -INFINITY;
 #pragma unroll
       for (int i = 0; i < LOADS; ++i) mx = fmaxf(mx, sc[i][r]);
-      const float mu = mx == -INFINITY ? 0.f : mx;
+      // Lazy running maximum (kLazyMax): alpha is exactly 1 unless it moved,
+      // and the rescale of the accumulator is skipped when no lane needs it.
+      const float mnew = mx > mrun[r] + kLazyMax ? mx : mrun[r];
+      const float mu = mnew == -INFINITY ? 0.f : mnew;
       const float alpha = fast_exp2(mrun[r] - mu);
       float pw[LOADS], ps = 0.f;
 #pragma unroll
@@ -514,9 +514,11 @@ __device__ void resp_unit(const AttnArgs& a, int item, int h, char* smem) {
         ps += pw[i];
       }
       l[r] = l[r] * alpha + ps;
-      mrun[r] = mx;
+      mrun[r] = mnew;
+      if (__any(alpha != 1.f)) {
 #pragma unroll
-      for (int e = 0; e < EPL; ++e) o[r][e] *= alpha;
+        for (int e = 0; e < EPL; ++e) o[r][e] *= alpha;
+      }
 #pragma unroll
       for (int i = 0; i < LOADS; ++i) {
         const float pv = pw[i] * vmul;

@@ -24,6 +24,11 @@ constexpr int kRespChunkPagesMax = 64;
 constexpr int kLongResponsePages = 256;
 
 constexpr float kLog2e = 1.4426950408889634f;
+// Headroom of a lazily updated softmax running maximum, in log2 units: the
+// maximum moves only when new scores exceed it by more than this, so the
+// weights exp2(s - m) stay below 2^8 and most updates leave the output
+// accumulator unscaled.
+constexpr float kLazyMax = 8.0f;
 constexpr float kLn2 = 0.6931471805599453f;
 
 // Plan header slots.

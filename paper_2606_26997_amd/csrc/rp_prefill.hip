@@ -117,7 +117,6 @@ __global__ __launch_bounds__(64) void prefill_kv_write_kernel(const PrefillArgs 
 constexpr int kPfWaves = 4;
 constexpr int kPfThreads = 64 * kPfWaves;
 constexpr int kKeyBlk = 32;
-constexpr float kLazyMax = 8.0f;  // headroom of the running softmax maximum, log2 units
 
 template <int D>
 struct PfSmem {
