@@ -133,7 +133,7 @@ __device__ inline uint32_t f32_to_e4m3(float x) {
 // amax <= 448 * old, and otherwise sets scale = amax / 448 after requantising
 // rows 0..r-1 from code * old. Plain IEEE fp32 (no contraction, correctly
 // rounded division), so the bytes are a deterministic function of the inputs.
-// Every lane of the wave must call it with the same r.
+// Every lane of a G-lane group must call it, with the same r.
 template <int D, int G, int N, class ColFn>
 __device__ void append_fp8_row(uint8_t* blk, float* scale_slot, int r, const float (&x)[N], ColFn col,
                                bool leader) {

@@ -317,7 +317,8 @@ __global__ __launch_bounds__(kPfThreads) void prefill_attn_kernel(const PrefillA
     const uint16_t* qrow = static_cast<const uint16_t*>(a.q) + (size_t)(first + min(tr[rt], last)) * qpitch +
                            (size_t)jr * D + quad * 8;
 #pragma unroll
-    for (int kb = 0; kb < KB; ++kb) qop[rt][kb] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(qrow + kb * 32));
+    for (int kb = 0; kb < KB; ++kb)
+      qop[rt][kb] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(qrow + kb * 32));
   }
 
   const int tlast = min(T0 + TPB, P) - 1;  // the workgroup's last token bounds its keys

@@ -13,11 +13,11 @@
 // Work split: a sequence has Hq + 2 Hkv head slots (q heads, k heads, v
 // heads); a group of 16 lanes owns one slot (or two, j and j + 16, on large
 // batches), a block of 256 threads 16 (32) slots of one sequence, all of
-// their loads in flight at once. Lane l of a group holds the D/32 pairs l*D/32 + p, that is
-// columns l*D/32 + p and D/2 + l*D/32 + p, so each pair is rotated in-lane and
-// every row is read and written as whole 16-lane runs. Each block computes
-// the cos/sin of the D/2 angles of its sequence once, folded with the norm
-// weights into LDS tables.
+// their loads in flight at once. Lane l of a group holds the D/32 pairs
+// l*D/32 + p, that is columns l*D/32 + p and D/2 + l*D/32 + p, so each pair
+// is rotated in-lane and every row is read and written as whole 16-lane
+// runs. Each block computes the cos/sin of the D/2 angles of its sequence
+// once, folded with the norm weights into LDS tables.
 #include "rp_device.h"
 #include "rp_internal.h"
 
@@ -29,16 +29,10 @@ constexpr int kPrepThreads = 256;
 constexpr int kGroups = kPrepThreads / kSlotLanes;
 
 // fp64 -> bf16 bits, one rounding to nearest even, in two steps: the fp32
-// rounding f of y, then f's own rounding to bf16 (gfx950's packed
-// conversion, nearest even). That is the single rounding of y except when f
-// lands exactly on a bf16 tie while y does not; then y's side of the tie
-// decides (bf16_tie_fix). bf16_tie reports that case.
-__device__ inline uint32_t pack_bf16_rne(float lo, float hi) {
-  typedef __bf16 bf16x2_v __attribute__((ext_vector_type(2)));
-  typedef float f32x2_v __attribute__((ext_vector_type(2)));
-  const f32x2_v v = {lo, hi};
-  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_v));
-}
+// rounding f of y, then f's own rounding to bf16 (pack_bf16x2, nearest
+// even). That is the single rounding of y except when f lands exactly on a
+// bf16 tie while y does not; then y's side of the tie decides
+// (bf16_tie_fix). bf16_tie reports that case.
 __device__ inline bool bf16_tie(float f) { return (__float_as_uint(f) & 0xFFFFu) == 0x8000u; }
 __device__ inline uint32_t bf16_tie_fix(double y, float f) {
   const uint32_t u = __float_as_uint(f);
@@ -123,8 +117,8 @@ __device__ inline void prep_slot(const QkPrepArgs& a, int s, int kind, int head,
     }
 #pragma unroll
     for (int k = 0; k < W; ++k) {
-      o1[k] = pack_bf16_rne(f1[2 * k], f1[2 * k + 1]);
-      o2[k] = pack_bf16_rne(f2[2 * k], f2[2 * k + 1]);
+      o1[k] = pack_bf16x2(f1[2 * k], f1[2 * k + 1]);
+      o2[k] = pack_bf16x2(f2[2 * k], f2[2 * k + 1]);
     }
     if (tie) {  // rare: some fp32 value sits exactly on a bf16 tie
 #pragma unroll
