@@ -151,12 +151,20 @@ __device__ void append_fp8_row(uint8_t* blk, float* scale_slot, int r, const flo
     scale = old;
   } else {
     scale = amax / 448.0f;
-    for (int rr = 0; rr < r; ++rr) {
-      uint8_t* row = blk + (size_t)rr * D;
+    // Requantise rows 0..r-1, four rows' codes in flight per memory round trip.
+    constexpr int kRows = 4;
+    for (int r0 = 0; r0 < r; r0 += kRows) {
+      uint32_t c[kRows][N];
 #pragma unroll
-      for (int e = 0; e < N; ++e) {
-        const float val = e4m3_to_f32(row[col(e)]) * old;
-        row[col(e)] = (uint8_t)f32_to_e4m3(val / scale);
+      for (int k = 0; k < kRows; ++k)
+#pragma unroll
+        for (int e = 0; e < N; ++e) c[k][e] = r0 + k < r ? blk[(size_t)(r0 + k) * D + col(e)] : 0u;
+#pragma unroll
+      for (int k = 0; k < kRows; ++k) {
+        if (r0 + k >= r) break;
+        uint8_t* row = blk + (size_t)(r0 + k) * D;
+#pragma unroll
+        for (int e = 0; e < N; ++e) row[col(e)] = (uint8_t)f32_to_e4m3(e4m3_to_f32(c[k][e]) * old / scale);
       }
     }
   }
