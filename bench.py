@@ -695,19 +695,22 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_per_step = wall / args.steps * 1e3
-    parts_us = float(np.mean([events[k][ip].elapsed_time(events[k][ip + 1])
-                              for k in range(args.steps)])) * 1e3
+    parts_samples = np.array([events[k][ip].elapsed_time(events[k][ip + 1]) for k in range(args.steps)]) * 1e3
+    parts_us = float(parts_samples.mean())
 
     # Untimed breakdown pass: events between every launch.
     events = new_events()
     for k in range(args.steps):
         step(events[k])
     torch.cuda.synchronize()
-    per_kernel = {name: float(np.mean([events[k][i].elapsed_time(events[k][i + 1])
-                                       for k in range(args.steps)])) * 1e3
-                  for i, name in enumerate(stages)}      # microseconds
-    event_step_us = float(np.mean([events[k][0].elapsed_time(events[k][-1])
-                                   for k in range(args.steps)])) * 1e3
+    samples = {name: np.array([events[k][i].elapsed_time(events[k][i + 1]) for k in range(args.steps)]) * 1e3
+               for i, name in enumerate(stages)}      # microseconds
+    samples["step"] = np.array([events[k][0].elapsed_time(events[k][-1]) for k in range(args.steps)]) * 1e3
+    per_kernel = {name: float(samples[name].mean()) for name in stages}
+    event_step_us = float(samples["step"].mean())
+    samples["parts_timed"] = parts_samples
+    spread = {name: {"median": round(float(np.median(v)), 2), "p10": round(float(np.percentile(v, 10)), 2),
+                     "p90": round(float(np.percentile(v, 90)), 2)} for name, v in samples.items()}
 
     gbps = bm["total"] / (ms_per_step * 1e-3) / 1e9
     achieved = bm["parts_kernel"] / (parts_us * 1e-6) / 1e9
@@ -741,6 +744,7 @@ def main():
         "kernel_us": {k: round(v, 2) for k, v in per_kernel.items()},
         "event_step_us": round(event_step_us, 2),
         "parts_kernel_us_timed": round(parts_us, 2),
+        "kernel_us_spread": spread,
         "roofline": {"kernel": "attn_parts_kernel", "bound": "hbm", "achieved": round(achieved, 2),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": traffic, "algorithmic_bytes_per_launch": int(bm["parts_kernel"])},

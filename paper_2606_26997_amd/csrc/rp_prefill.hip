@@ -218,6 +218,15 @@ __device__ __forceinline__ void pf_compute(const uint16_t* kst, int u0, int last
       for (int rt = 0; rt < RT; ++rt) sacc[rt][st] = mfma16x16x32(kop, qop[rt][kb], sacc[rt][st]);
     }
   }
+  // V^T operands of the whole block, read while the softmax runs.
+  bf16x8_t vop[DT];
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt) {
+    const uint16_t* vrow = vst + (dt * 16 + r16) * L::kVPitch + quad * 4;
+    const bf16x4_t v0 = __builtin_bit_cast(bf16x4_t, *reinterpret_cast<const uint2*>(vrow));
+    const bf16x4_t v1 = __builtin_bit_cast(bf16x4_t, *reinterpret_cast<const uint2*>(vrow + 16));
+    vop[dt] = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
+  }
   bf16x4_t pop[RT][ST];
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt) {
@@ -272,12 +281,8 @@ __device__ __forceinline__ void pf_compute(const uint16_t* kst, int u0, int last
     pop8[rt] = __builtin_shufflevector(pop[rt][0], pop[rt][1], 0, 1, 2, 3, 4, 5, 6, 7);
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt) {
-    const uint16_t* vrow = vst + (dt * 16 + r16) * L::kVPitch + quad * 4;
-    const bf16x4_t v0 = __builtin_bit_cast(bf16x4_t, *reinterpret_cast<const uint2*>(vrow));
-    const bf16x4_t v1 = __builtin_bit_cast(bf16x4_t, *reinterpret_cast<const uint2*>(vrow + 16));
-    const bf16x8_t vop = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
 #pragma unroll
-    for (int rt = 0; rt < RT; ++rt) oacc[rt][dt] = mfma16x16x32(vop, pop8[rt], oacc[rt][dt]);
+    for (int rt = 0; rt < RT; ++rt) oacc[rt][dt] = mfma16x16x32(vop[dt], pop8[rt], oacc[rt][dt]);
   }
 }
 
