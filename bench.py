@@ -51,6 +51,8 @@ def parse_args():
     p.add_argument("--seed", type=int, default=None)
     p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="wall-clock budget of the oracle CPU baseline sample (0 disables it)")
+    p.add_argument("--read-ceiling", action="store_true",
+                   help="time plain torch streaming kernels (4 GiB sum, 1 GiB copy) as roofline context")
     p.add_argument("--copy-calibration", action="store_true",
                    help="run only a plain device copy of known size (for HBM counter scaling)")
     p.add_argument("--prefill", action="store_true",
@@ -107,6 +109,11 @@ def byte_model(wl):
     # The partial-attention kernel reads every K/V page once, their scales and q.
     out["parts_kernel"] = out["prefix_kv"] + out["resp_kv"] + scale_bytes + q_bytes
     out["prefix_tokens"], out["resp_tokens"] = prefix_tokens, resp_tokens
+    # The group-prefix MFMA tile: live(g) * n_rep query rows per (group, kv-head), in 16-row tiles.
+    rows = np.bincount(wl.seq_to_group, minlength=wl.num_groups)[live] * (Hq // Hkv)
+    tile_rows = 16 * ((rows + 15) // 16)
+    out["prefix_tile_rows"] = int(rows.sum())
+    out["prefix_tile_padded_frac"] = float(1.0 - rows.sum() / tile_rows.sum()) if tile_rows.sum() else 0.0
     return out
 
 
@@ -200,6 +207,32 @@ def copy_calibration(steps):
     el = (time.perf_counter() - t0) / steps
     print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "ms": el * 1e3,
                       "GBps_read_plus_write": 2 * n / el / 1e9}), flush=True)
+
+
+def read_ceiling(steps):
+    """Context for the roofline: plain streaming kernels of torch on this GPU, median over steps.
+    A 4 GiB sum (read only) and a 1 GiB copy (read + write); both exceed the 256 MB last-level cache."""
+    import numpy as np
+    import torch
+    x = torch.ones(1 << 31, dtype=torch.bfloat16, device="cuda")      # 4 GiB
+    a = torch.ones(1 << 30, dtype=torch.uint8, device="cuda")
+    b = torch.empty_like(a)
+    res = {}
+    for name, fn, nbytes in (("sum_read", lambda: x.sum(dtype=torch.float32), x.numel() * 2),
+                             ("copy_read_write", lambda: b.copy_(a), 2 * a.numel())):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+        for e0, e1 in ev:
+            e0.record()
+            fn()
+            e1.record()
+        torch.cuda.synchronize()
+        ms = float(np.median([e0.elapsed_time(e1) for e0, e1 in ev]))
+        res[name] = {"bytes": nbytes, "ms": round(ms, 4), "GBps": round(nbytes / ms / 1e6, 1),
+                     "frac_of_8TBps": round(nbytes / ms / 1e6 / HBM_PEAK_GBPS, 4)}
+    print(json.dumps({"read_ceiling": res}), flush=True)
 
 
 def prefill_bench(args):
@@ -626,7 +659,7 @@ def grpo_bench(args):
 def main():
     args = parse_args()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
+        print(f"bench.py runs on one GPU; --gpus {args.gpus} is not supported "
               f"(the attention shards exchange-free by whole groups, see the design notes).",
               file=sys.stderr)
         sys.exit(2)
@@ -635,6 +668,9 @@ def main():
 
     if args.copy_calibration:
         copy_calibration(args.steps)
+        return
+    if args.read_ceiling:
+        read_ceiling(args.steps)
         return
     if args.traffic_from:
         summarise_traffic(args.traffic_from)
@@ -741,6 +777,7 @@ def main():
         "pct_of_hbm_peak": round(100.0 * gbps / HBM_PEAK_GBPS, 2),
         "seq_steps_per_s": round(wl.num_seqs / (ms_per_step * 1e-3), 1),
         "algorithmic_bytes_per_step": int(bm["total"]),
+        "prefix_tile_padded_rows_frac": round(bm["prefix_tile_padded_frac"], 4),
         "kernel_us": {k: round(v, 2) for k, v in per_kernel.items()},
         "event_step_us": round(event_step_us, 2),
         "parts_kernel_us_timed": round(parts_us, 2),
