@@ -228,9 +228,11 @@ rp_status rp_prefill_attn(const rp_paged_kv* kv, const rp_prefill_layout* layout
 /* Build the work plan in `workspace` from the layout's device arrays: group
  * member lists, prefix work items (16-page chunks of each live group's
  * prefix), response work items (every response cut into pieces of B pages,
- * B = 32 or 64 chosen per batch from the average response length, the
- * B-page pieces first and then each response's shorter last piece by
- * decreasing size), and the number of partial results per query row.
+ * the B-page pieces first and then each response's shorter last piece by
+ * decreasing size), and the number of partial results per query row. B is
+ * the multiple of 32 pages nearest to W / (32 * 6 * C), clamped to 32..128,
+ * where W is the batch's response pages (ceil(resp_lens[s] / 16) summed over
+ * s) times num_kv_heads and C the current device's compute units.
  * Must be re-run whenever seq_to_group, prefix_lens or resp_lens change.
  * Supports num_groups <= 4096. */
 rp_status rp_plan(const rp_paged_kv* kv, const rp_group_layout* layout,

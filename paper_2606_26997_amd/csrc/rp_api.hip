@@ -131,6 +131,24 @@ bool ws_layout(const Shape& sh, WsLayout* w) {
   return true;
 }
 
+// Compute units of the current device, queried once per device (racing first
+// calls store the same value).
+rp_status device_cus(int* cus) {
+  static int cache[64] = {0};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= 64) return fail(RP_ERR_UNSUPPORTED, "device %d out of range", dev);
+  if (cache[dev] == 0) {
+    int n = 0;
+    e = hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute");
+    cache[dev] = n;
+  }
+  *cus = cache[dev];
+  return RP_OK;
+}
+
 rp::PlanView plan_view(void* ws, const WsLayout& w) {
   char* b = static_cast<char*>(ws);
   rp::PlanView v;
@@ -227,10 +245,15 @@ rp_status rp_plan(const rp_paged_kv* kv, const rp_group_layout* l, void* ws, siz
   WsLayout w;
   rp_status st = prepare(kv, l, ws, ws_bytes, &sh, &w);
   if (st != RP_OK || sh.S == 0) return st;
+  int cus = 0;
+  st = device_cus(&cus);
+  if (st != RP_OK) return st;
   rp::PlanArgs a;
   a.num_seqs = sh.S;
   a.num_groups = sh.G;
   a.num_q_heads = sh.Hq;
+  a.num_kv_heads = sh.Hkv;
+  a.num_cus = cus;
   a.seq_to_group = l->seq_to_group;
   a.prefix_lens = l->prefix_lens;
   a.resp_lens = l->resp_lens;

@@ -13,15 +13,21 @@ constexpr int kPage = 16;
 // a response of P pages becomes floor(P / B) pieces of B pages and, if P is
 // not a multiple of B, one ragged piece with the rest. Items are dispatched
 // largest first (all B-sized pieces, then the ragged ones by decreasing
-// size). The planner picks B per batch: kRespChunkPagesMin when the average
-// response is below kLongResponsePages pages, else kRespChunkPagesMax; large
-// pieces amortise each unit's start-up latency, and measured alternatives
-// with extra small pieces at the end cost more start-ups than they saved.
-// Workspace is sized for the smaller B.
+// size). The planner picks B per batch among kRespChunkStep, 2x, 3x and 4x
+// that (32 to 128 pages): the multiple of kRespChunkStep nearest to
+// W / (kRespChunkStep * kUnitsPerCu * compute units), W being the batch's
+// response pages times its kv-heads, so that a batch has about kUnitsPerCu
+// B-sized units per compute unit or more. Long pieces amortise each unit's
+// start-up latency on big batches; small batches keep enough units in flight
+// to fill the memory pipeline. Measured alternatives with extra small pieces
+// at the end cost more start-ups than they saved. Workspace is sized for the
+// smallest B.
 constexpr int kPrefixChunkPages = 16;
-constexpr int kRespChunkPagesMin = 32;
-constexpr int kRespChunkPagesMax = 64;
-constexpr int kLongResponsePages = 256;
+constexpr int kRespChunkStep = 32;
+constexpr int kRespChunkChoices = 4;
+constexpr int kRespChunkPagesMin = kRespChunkStep;
+constexpr int kRespChunkPagesMax = kRespChunkStep * kRespChunkChoices;
+constexpr int kUnitsPerCu = 6;
 
 constexpr float kLog2e = 1.4426950408889634f;
 // Headroom of a lazily updated softmax running maximum, in log2 units: the

@@ -24,7 +24,8 @@ __device__ inline int clamp_page(int p, int num_pages) {
 }
 
 struct PlanArgs {
-  int num_seqs, num_groups, num_q_heads;
+  int num_seqs, num_groups, num_q_heads, num_kv_heads;
+  int num_cus;  // compute units of the device the batch runs on (sets the piece length)
   const int* seq_to_group;
   const int* prefix_lens;
   const int* resp_lens;

@@ -2,7 +2,7 @@
 //  * per-group member lists (CSR over sequences),
 //  * prefix work items (group, chunk of kPrefixChunkPages prefix pages) for
 //    groups with at least one live member,
-//  * the piece length B for this batch (from the average response length),
+//  * the piece length B for this batch (from its total response pages),
 //  * the number of partial results per query row of each sequence,
 //  * response work items (sequence, first page, tokens, partial-result slot):
 //    every B-page piece first, then the ragged last pieces by decreasing size.
@@ -71,9 +71,9 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
   __shared__ int s_sl[kPlanSeqBlock];     // clamped response length of each sequence of the pass
   __shared__ int s_off[kPlanSeqBlock];    // first B-sized piece of each sequence of the pass
   __shared__ int s_own[kRoundItems];      // sequence (of the pass) of each B-sized piece of a round
-  __shared__ int s_hist[2][kRespChunkPagesMax];  // ragged pieces per page count, for B = min and max
-  __shared__ int s_hoff[kRespChunkPagesMax];     // next item index per ragged page count
-  __shared__ int s_nbig[2];                      // B-sized pieces, for B = min and max
+  __shared__ int s_hist[kRespChunkPagesMax];  // ragged pieces per page count
+  __shared__ int s_hoff[kRespChunkPagesMax];  // next item index per ragged page count
+  __shared__ int s_nbig;                      // B-sized pieces
   __shared__ long long s_tot[kPlanWaves];
   __shared__ unsigned long long s_pages;
   const int t = threadIdx.x, lane = t & 63;
@@ -81,17 +81,18 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
   const PlanView v = a.view;
 
   for (int g = t; g < G; g += kPlanThreads) s_cnt[g] = 0;
-  if (t < 2 * kRespChunkPagesMax) s_hist[t / kRespChunkPagesMax][t % kRespChunkPagesMax] = 0;
-  if (t < 2) s_nbig[t] = 0;
-  if (t == 0) s_pages = 0;
+  if (t < kRespChunkPagesMax) s_hist[t] = 0;
+  if (t == 0) {
+    s_nbig = 0;
+    s_pages = 0;
+  }
   __syncthreads();
 
-  // One pass over the inputs: group sizes, prefix chunks per group, total
-  // response pages, and the piece counts for both piece lengths.
+  // First pass over the inputs: group sizes, prefix chunks per group and the
+  // total response pages, which set B.
   for (int g = t; g < G; g += kPlanThreads)
     s_gpc[g] = prefix_chunks(a.prefix_lens[g], a.max_prefix_pages, v.max_prefix_chunks);
   unsigned long long my_pages = 0;
-  int my_big[2] = {0, 0};
   for (int s = t; s < S; s += kPlanThreads) {
     const int g = clamp_group(a.seq_to_group[s], G);
     const int L = clamp_len(a.resp_lens[s], a.max_resp_pages);
@@ -100,33 +101,42 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
       s_sl[s] = L;
     }
     atomicAdd(&s_cnt[g], 1);
-    const int pages = cdiv(L, kPage);
-    my_pages += pages;
-    my_big[0] += pages / kRespChunkPagesMin;
-    my_big[1] += pages / kRespChunkPagesMax;
-    if (pages % kRespChunkPagesMin) atomicAdd(&s_hist[0][pages % kRespChunkPagesMin], 1);
-    if (pages % kRespChunkPagesMax) atomicAdd(&s_hist[1][pages % kRespChunkPagesMax], 1);
+    my_pages += cdiv(L, kPage);
   }
   // One LDS atomic per wave: same-address atomics from every thread serialise.
   my_pages = (unsigned long long)wave_sum((long long)my_pages);
-  const long long big = wave_sum(pack2(my_big[0], my_big[1]));
-  if (lane == 0) {
-    atomicAdd(&s_pages, my_pages);
-    atomicAdd(&s_nbig[0], hi32(big));
-    atomicAdd(&s_nbig[1], lo32(big));
-  }
+  if (lane == 0) atomicAdd(&s_pages, my_pages);
   __syncthreads();
-  const int lc = s_pages >= (unsigned long long)S * kLongResponsePages ? 1 : 0;
-  const int chunk = lc ? kRespChunkPagesMax : kRespChunkPagesMin;
-  const int nbig = s_nbig[lc];
+  // B: the multiple of kRespChunkStep nearest to W / (kRespChunkStep * target
+  // units), W = response pages x kv-heads, clamped to the candidates.
+  const long long W = (long long)s_pages * a.num_kv_heads;
+  const long long unit = (long long)kRespChunkStep * kUnitsPerCu * max(a.num_cus, 1);
+  const int chunk = kRespChunkStep * (int)min(max((W + unit / 2) / unit, 1ll), (long long)kRespChunkChoices);
+
+  // Second pass (lengths from LDS where the first pass kept them): B-sized
+  // pieces and the ragged pieces per page count.
+  int my_big = 0;
+  for (int s = t; s < S; s += kPlanThreads) {
+    const int L = s < kPlanSeqBlock ? s_sl[s] : clamp_len(a.resp_lens[s], a.max_resp_pages);
+    const int pages = cdiv(L, kPage);
+    my_big += pages / chunk;
+    if (pages % chunk) atomicAdd(&s_hist[pages % chunk], 1);
+  }
+  my_big = (int)wave_sum(my_big);
+  if (lane == 0) atomicAdd(&s_nbig, my_big);
+  __syncthreads();
+  const int nbig = s_nbig;
 
   // Item order: every B-sized piece first, then the ragged pieces by
-  // decreasing page count (one wave scans the count bins, largest first).
+  // decreasing page count (one wave scans the count bins, largest first, two
+  // bins per lane).
+  static_assert(kRespChunkPagesMax <= 128, "one wave scans the piece-count bins");
   if (t < 64) {
-    const int r = chunk - 1 - lane;
-    const int h = r >= 1 ? s_hist[lc][r] : 0;
-    const int incl = (int)wave_incl_scan(h, lane);
-    if (r >= 1) s_hoff[r] = nbig + incl - h;
+    const int r1 = chunk - 1 - 2 * lane, r0 = r1 - 1;
+    const int h1 = r1 >= 1 ? s_hist[r1] : 0, h0 = r0 >= 1 ? s_hist[r0] : 0;
+    const int incl = (int)wave_incl_scan(h1 + h0, lane);
+    if (r1 >= 1) s_hoff[r1] = nbig + incl - h1 - h0;
+    if (r0 >= 1) s_hoff[r0] = nbig + incl - h0;
     if (lane == 63) {
       v.hdr[kHdrRespItems] = nbig + incl;
       v.hdr[kHdrBigRespItems] = nbig;

@@ -43,10 +43,10 @@ RAGGED = [
     ("no-prefix", 4, 2, 128, [0, 0], [0], [40, 1], "bf16"),
     ("fp8-edges", 16, 8, 128, [0, 0, 1, 1, 1], [33, 200], [0, 16, 17, 300, 513], "fp8"),
     ("fp8-d64-nrep4", 8, 2, 64, [0, 1, 0], [64, 9], [100, 31, 0], "fp8"),
-    # Response lengths on both sides of 32-page piece boundaries (short pieces).
+    # Response lengths on both sides of 32-page piece boundaries.
     ("piece-edges-short", 4, 2, 64, [0] * 5 + [1] * 4, [20, 0],
      [497, 500, 511, 512, 513, 1008, 1009, 1023, 1024], "bf16"),
-    # Average above 256 pages, so 64-page pieces, with lengths at their edges.
+    # Lengths at the edges of 64-page multiples (32-page pieces: the batch is small).
     ("piece-edges-long", 4, 2, 64, [0, 0, 0, 1, 1, 1, 1], [100, 16],
      [4090, 4096, 4097, 8191, 8192, 1000, 12000], "bf16"),
 ]
@@ -281,4 +281,26 @@ def test_full_config_sampled_rows(cid):
     seqs = sorted(picks)
     ref_out, ref_lse, _ = run_oracle(wl, seqs=seqs)
     compare(out[seqs], lse[seqs], ref_out, ref_lse, wl.kv_dtype, f"config{cid}")
+    assert np.isfinite(out).all() and np.isfinite(lse).all()
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("lo,hi,pages", [(2500, 3500, 64), (3800, 4400, 96)])
+def test_frontier_batches_with_longer_pieces(lo, hi, pages):
+    """8 groups x 8 live sequences: the planner picks 64- or 96-page pieces on a 256-CU GPU. Lengths
+    include the edges of those multiples; oracle on sampled sequences, including every edge one."""
+    import paper_2606_26997_amd as rp
+    _say(f"frontier 64 seqs, responses U[{lo}, {hi}]")
+    rng = np.random.default_rng(lo)
+    L = rng.integers(lo, hi + 1, 64)
+    edges = [pages * 16 * k + e for k in (2, 3) for e in (-1, 0, 1)]
+    L[:len(edges)] = edges
+    wl = make_workload(num_q_heads=16, num_kv_heads=8, head_dim=128, seq_to_group=np.repeat(np.arange(8), 8),
+                       prefix_lens=rng.integers(64, 513, 8), resp_lens=L, seed=lo)
+    batch, out, lse = run_hip(wl)
+    if torch.cuda.get_device_properties(0).multi_processor_count == 256:
+        assert int(batch.plan_contents()["hdr"][3]) == pages
+    seqs = sorted(set(range(len(edges))) | set(rng.choice(64, size=8, replace=False).tolist()))
+    ref_out, ref_lse, _ = run_oracle(wl, seqs=seqs)
+    compare(out[seqs], lse[seqs], ref_out, ref_lse, "bf16", f"frontier-{pages}")
     assert np.isfinite(out).all() and np.isfinite(lse).all()

@@ -15,7 +15,17 @@ import torch
 
 pytestmark = pytest.mark.gpu
 
-PAGE, PREFIX_CHUNK, B_MIN, B_MAX, LONG_PAGES = 16, 16, 32, 64, 256
+PAGE, PREFIX_CHUNK = 16, 16
+B_STEP, B_CHOICES, UNITS_PER_CU = 32, 4, 6
+HKV = 8
+
+
+def piece_pages(pages, hkv, cus):
+    """The contract's piece length: the multiple of 32 pages nearest to W / (32 * 6 * compute units),
+    W = response pages x kv-heads, clamped to 32..128."""
+    W = int(pages.sum()) * hkv
+    unit = B_STEP * UNITS_PER_CU * cus
+    return B_STEP * min(max((W + unit // 2) // unit, 1), B_CHOICES)
 
 
 def cdiv(a, b):
@@ -47,7 +57,7 @@ def check_plan(b, s2g, P, L, rbt, G):
     got = b.plan_contents()
     hdr = got["hdr"]
     pages = cdiv(L, PAGE)
-    B = B_MAX if pages.sum() >= S * LONG_PAGES else B_MIN
+    B = piece_pages(pages, HKV, torch.cuda.get_device_properties(0).multi_processor_count)
     assert hdr[3] == B
     live = np.bincount(s2g, minlength=G)
     npc = cdiv(cdiv(P, PAGE), PREFIX_CHUNK)
@@ -75,8 +85,8 @@ def check_plan(b, s2g, P, L, rbt, G):
     tail_pages = cdiv(tail[:, 2].astype(np.int64), PAGE)
     assert np.all(np.diff(tail_pages) <= 0), "last pieces must come by decreasing page count"
     assert np.all(tail_pages < B)
-    return B
     assert np.array_equal(got["seq_parts"], npc[s2g] + cdiv(pages, B))
+    return B
 
 
 def _case(name):
@@ -110,7 +120,15 @@ def _case(name):
         G, S = 2, 16
         s2g = np.repeat(np.arange(G), 8)
         P, L = rng.integers(64, 513, G), rng.integers(3000, 4001, S)
-    elif name == "few-long-sequences":      # average >= 256 pages over only 8 sequences
+    elif name == "frontier-dispatch-64":    # 8 groups x 8 live sequences, ~190 pages each
+        G, S = 8, 64
+        s2g = np.repeat(np.arange(G), 8)
+        P, L = rng.integers(64, 513, G), rng.integers(2500, 3501, S)
+    elif name == "frontier-dispatch-64-long":  # 8 groups x 8 live sequences, ~256 pages each
+        G, S = 8, 64
+        s2g = np.repeat(np.arange(G), 8)
+        P, L = rng.integers(64, 513, G), rng.integers(3800, 4401, S)
+    elif name == "few-long-sequences":      # long responses, but only 8 of them
         G, S = 2, 8
         s2g = np.repeat(np.arange(G), 4)
         P, L = np.array([100, 300]), rng.integers(6000, 9000, S)
@@ -124,7 +142,8 @@ def _case(name):
 
 
 CASES = ["qwen-layer-uniform", "lognormal-tail", "frontier-random-map", "long-context", "many-sequences",
-         "many-pieces", "frontier-dispatch-16", "few-long-sequences", "empty-and-idle-groups"]
+         "many-pieces", "frontier-dispatch-16", "frontier-dispatch-64", "frontier-dispatch-64-long",
+         "few-long-sequences", "empty-and-idle-groups"]
 
 
 @pytest.mark.parametrize("name", CASES)
@@ -134,9 +153,9 @@ def test_plan_matches_its_contract(name):
     G, s2g, P, L = _case(name)
     b, rbt = make_batch(s2g, P, L, G, seed=len(name))
     B = check_plan(b, s2g, P, L, rbt, G)
-    if name in ("qwen-layer-uniform", "lognormal-tail", "frontier-dispatch-16"):
-        assert B == 32, B
-    if name in ("frontier-random-map", "long-context", "few-long-sequences"):
-        assert B == 64, B
+    if torch.cuda.get_device_properties(0).multi_processor_count == 256:   # MI355X: every candidate B occurs
+        want = {"frontier-dispatch-16": 32, "few-long-sequences": 32, "empty-and-idle-groups": 32,
+                "frontier-dispatch-64": 64, "frontier-dispatch-64-long": 96}.get(name, 128)
+        assert B == want, (name, B)
     # A second plan into the same workspace gives the same B-page items.
     check_plan(b, s2g, P, L, rbt, G)
