@@ -232,7 +232,10 @@ rp_status rp_prefill_attn(const rp_paged_kv* kv, const rp_prefill_layout* layout
  * decreasing size), and the number of partial results per query row. B is
  * the multiple of 32 pages nearest to W / (32 * 6 * C), clamped to 32..128,
  * where W is the batch's response pages (ceil(resp_lens[s] / 16) summed over
- * s) times num_kv_heads and C the current device's compute units.
+ * s) times num_kv_heads and C the current device's compute units; it is 16
+ * when W < 0.75 * 32 * 6 * C and the layout's response capacity (num_seqs *
+ * max_resp_pages * num_kv_heads) is at most 2^17 page-heads, the layouts
+ * whose workspace is sized for 16-page pieces.
  * Must be re-run whenever seq_to_group, prefix_lens or resp_lens change.
  * Supports num_groups <= 4096. */
 rp_status rp_plan(const rp_paged_kv* kv, const rp_group_layout* layout,

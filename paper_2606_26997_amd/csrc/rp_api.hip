@@ -110,7 +110,8 @@ size_t align_up(size_t x) { return (x + 255) & ~size_t(255); }
 
 bool ws_layout(const Shape& sh, WsLayout* w) {
   w->max_pc = rp::cdiv(sh.max_pp, rp::kPrefixChunkPages);
-  w->max_rc = rp::cdiv(sh.max_rp, rp::kRespChunkPagesMin);
+  const bool small = (long long)sh.S * sh.max_rp * sh.Hkv <= rp::kSmallBatchPageHeads;
+  w->max_rc = rp::cdiv(sh.max_rp, small ? rp::kRespChunkPagesSmall : rp::kRespChunkPagesMin);
   const long long groups_used = sh.G < sh.S ? sh.G : sh.S;
   w->max_pitems = groups_used * w->max_pc;
   w->max_ritems = (long long)sh.S * w->max_rc;

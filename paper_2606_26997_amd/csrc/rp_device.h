@@ -20,14 +20,19 @@ constexpr int kPage = 16;
 // B-sized units per compute unit or more. Long pieces amortise each unit's
 // start-up latency on big batches; small batches keep enough units in flight
 // to fill the memory pipeline. Measured alternatives with extra small pieces
-// at the end cost more start-ups than they saved. Workspace is sized for the
-// smallest B.
+// at the end cost more start-ups than they saved. Batches whose work is below
+// three quarters of one 32-page step take 16-page pieces instead, when the
+// workspace was sized for them: a layout with at most
+// kSmallBatchPageHeads page-heads of response capacity (sequences x table
+// width x kv-heads) is sized for 16-page pieces, any other for 32.
 constexpr int kPrefixChunkPages = 16;
 constexpr int kRespChunkStep = 32;
 constexpr int kRespChunkChoices = 4;
+constexpr int kRespChunkPagesSmall = 16;
 constexpr int kRespChunkPagesMin = kRespChunkStep;
 constexpr int kRespChunkPagesMax = kRespChunkStep * kRespChunkChoices;
 constexpr int kUnitsPerCu = 6;
+constexpr long long kSmallBatchPageHeads = 1ll << 17;
 
 constexpr float kLog2e = 1.4426950408889634f;
 // Headroom of a lazily updated softmax running maximum, in log2 units: the

@@ -111,7 +111,11 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
   // units), W = response pages x kv-heads, clamped to the candidates.
   const long long W = (long long)s_pages * a.num_kv_heads;
   const long long unit = (long long)kRespChunkStep * kUnitsPerCu * max(a.num_cus, 1);
-  const int chunk = kRespChunkStep * (int)min(max((W + unit / 2) / unit, 1ll), (long long)kRespChunkChoices);
+  int chunk = kRespChunkStep * (int)min(max((W + unit / 2) / unit, 1ll), (long long)kRespChunkChoices);
+  // Below three quarters of one step, 16-page pieces if every response fits
+  // the workspace's partial-result slots at that length.
+  if (4 * W < 3 * unit && v.max_resp_chunks >= cdiv(a.max_resp_pages, kRespChunkPagesSmall))
+    chunk = kRespChunkPagesSmall;
 
   // Second pass (lengths from LDS where the first pass kept them): B-sized
   // pieces and the ragged pieces per page count.

@@ -167,13 +167,17 @@ def test_plan_layout_sections_fit_the_workspace():
             info.seq_parts, info.part_o, info.part_lse]
     assert offs == sorted(offs) and len(set(offs)) == len(offs)
     assert all(o % 256 == 0 for o in offs)
-    # Capacities: 16-page prefix chunks, 32-page response pieces (the shorter B).
+    # Capacities: 16-page prefix chunks; response pieces of 16 pages, the shortest B, since this
+    # layout's response capacity (5 sequences x 70 pages x 2 kv-heads) is at most 2^17 page-heads.
     assert info.max_prefix_items == 2 * 1
-    assert info.max_resp_items == 5 * 3
-    assert info.parts_per_row == 1 + 3
-    assert info.max_parts == 5 * 4 * 4
+    assert info.max_resp_items == 5 * 5
+    assert info.parts_per_row == 1 + 5
+    assert info.max_parts == 5 * 4 * 6
     assert info.part_lse + 4 * info.max_parts <= need
     assert info.part_o + 4 * info.max_parts * 64 <= info.part_lse
+    # Above 2^17 page-heads the slots are sized for 32-page pieces.
+    big = B.plan_layout(kv, _layout(num_seqs=1000, num_groups=2, mpp=3, mrp=70))
+    assert big.max_resp_items == 1000 * 3 and big.parts_per_row == 1 + 3
     with pytest.raises(B.RpError):
         B.plan_layout(_kv(head_dim=96), lay)
 

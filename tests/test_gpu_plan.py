@@ -20,12 +20,19 @@ B_STEP, B_CHOICES, UNITS_PER_CU = 32, 4, 6
 HKV = 8
 
 
-def piece_pages(pages, hkv, cus):
+SMALL_B, SMALL_CAPACITY = 16, 1 << 17
+
+
+def piece_pages(pages, hkv, cus, table_width):
     """The contract's piece length: the multiple of 32 pages nearest to W / (32 * 6 * compute units),
-    W = response pages x kv-heads, clamped to 32..128."""
+    W = response pages x kv-heads, clamped to 32..128; 16 pages instead when W is below three quarters of
+    that step and the workspace was sized for 16-page pieces (sequences x table width x kv-heads <= 2^17)."""
     W = int(pages.sum()) * hkv
     unit = B_STEP * UNITS_PER_CU * cus
-    return B_STEP * min(max((W + unit // 2) // unit, 1), B_CHOICES)
+    B = B_STEP * min(max((W + unit // 2) // unit, 1), B_CHOICES)
+    if 4 * W < 3 * unit and len(pages) * table_width * hkv <= SMALL_CAPACITY:
+        B = SMALL_B
+    return B
 
 
 def cdiv(a, b):
@@ -57,7 +64,7 @@ def check_plan(b, s2g, P, L, rbt, G):
     got = b.plan_contents()
     hdr = got["hdr"]
     pages = cdiv(L, PAGE)
-    B = piece_pages(pages, HKV, torch.cuda.get_device_properties(0).multi_processor_count)
+    B = piece_pages(pages, HKV, torch.cuda.get_device_properties(0).multi_processor_count, rbt.shape[1])
     assert hdr[3] == B
     live = np.bincount(s2g, minlength=G)
     npc = cdiv(cdiv(P, PAGE), PREFIX_CHUNK)
@@ -154,7 +161,7 @@ def test_plan_matches_its_contract(name):
     b, rbt = make_batch(s2g, P, L, G, seed=len(name))
     B = check_plan(b, s2g, P, L, rbt, G)
     if torch.cuda.get_device_properties(0).multi_processor_count == 256:   # MI355X: every candidate B occurs
-        want = {"frontier-dispatch-16": 32, "few-long-sequences": 32, "empty-and-idle-groups": 32,
+        want = {"frontier-dispatch-16": 16, "few-long-sequences": 16, "empty-and-idle-groups": 16,
                 "frontier-dispatch-64": 64, "frontier-dispatch-64-long": 96}.get(name, 128)
         assert B == want, (name, B)
     # A second plan into the same workspace gives the same B-page items.
