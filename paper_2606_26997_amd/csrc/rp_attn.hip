@@ -19,8 +19,9 @@
 // DPP, every group of LPT lanes keeps its own online-softmax state, and the
 // states are merged once per unit. Page loads are software-pipelined: the next
 // page's K is requested as soon as this page's scores exist and its V as soon as
-// this page's V is unpacked. How responses split into items is the planner's
-// choice for the batch.
+// this page's V is unpacked (for fp8 pools, whose blocks are half the bytes, the
+// page two ahead, so that two pages are in flight). How responses split into
+// items is the planner's choice for the batch.
 //
 // Each unit writes one partial (o normalised, lse natural-log) per query row
 // into its fixed slot (row, chunk); the combine kernel merges a row's parts.
@@ -449,15 +450,18 @@ __device__ void resp_unit(const AttnArgs& a, int item, int h, char* smem) {
     for (int e = 0; e < EPL; ++e) o[r][e] = 0.f;
   }
 
-  for (int p = wave; p < npages; p += kUnitWaves) {
-    // This wave's following page (this one again after its last: a cache hit).
-    const int next_page = p + kUnitWaves < npages ? clamp_page(bt[p + kUnitWaves], a.num_pages) : page;
+  // One page: scores from the K registers, which are then refilled with the
+  // page `ahead` pages on (this page again past the unit's end: a cache hit),
+  // V unpacked and refilled the same way, then the online softmax and P V.
+  const auto step = [&](int p, int ahead, int& pg, uint4 (&kx)[LOADS], uint4 (&vx)[LOADS])
+                        __attribute__((always_inline)) {
+    const int next_page = p + ahead < npages ? clamp_page(bt[p + ahead], a.num_pages) : pg;
     const size_t next_blk = resp_block<D, FP8>(a, next_page, h, lane);
     const int nvalid = min(kPage, ntok - p * kPage);
     float smul = a.qk_scale, vmul = 1.f;
     if constexpr (FP8) {
-      smul *= a.k_scale[(size_t)page * Hkv + h];
-      vmul = a.v_scale[(size_t)page * Hkv + h];
+      smul *= a.k_scale[(size_t)pg * Hkv + h];
+      vmul = a.v_scale[(size_t)pg * Hkv + h];
     }
 
     float sc[LOADS][NREP];
@@ -465,26 +469,26 @@ __device__ void resp_unit(const AttnArgs& a, int item, int h, char* smem) {
     for (int i = 0; i < LOADS; ++i) {
       if constexpr (!FP8) {
 #pragma unroll
-        for (int r = 0; r < NREP; ++r) sc[i][r] = group_sum<LPT>(dot8_bf16(qb[r][0], kr[i], 0.f)) * smul;
+        for (int r = 0; r < NREP; ++r) sc[i][r] = group_sum<LPT>(dot8_bf16(qb[r][0], kx[i], 0.f)) * smul;
       } else {
-        const uint4 k0 = e4m3x8_to_bf16x8(kr[i].x, kr[i].y);
-        const uint4 k1 = e4m3x8_to_bf16x8(kr[i].z, kr[i].w);
+        const uint4 k0 = e4m3x8_to_bf16x8(kx[i].x, kx[i].y);
+        const uint4 k1 = e4m3x8_to_bf16x8(kx[i].z, kx[i].w);
 #pragma unroll
         for (int r = 0; r < NREP; ++r)
           sc[i][r] = group_sum<LPT>(dot8_bf16(qb[r][1], k1, dot8_bf16(qb[r][0], k0, 0.f))) * smul;
       }
     }
 #pragma unroll
-    for (int i = 0; i < LOADS; ++i) kr[i] = *reinterpret_cast<const uint4*>(kpool + next_blk + i * 1024);
+    for (int i = 0; i < LOADS; ++i) kx[i] = *reinterpret_cast<const uint4*>(kpool + next_blk + i * 1024);
 
     float vf[LOADS][EPL];
 #pragma unroll
     for (int i = 0; i < LOADS; ++i) {
-      if constexpr (!FP8) unpack_bf16x8(vr[i], vf[i]);
-      else unpack_e4m3x16(vr[i], vf[i]);
+      if constexpr (!FP8) unpack_bf16x8(vx[i], vf[i]);
+      else unpack_e4m3x16(vx[i], vf[i]);
     }
 #pragma unroll
-    for (int i = 0; i < LOADS; ++i) vr[i] = load_v_stream(vpool + next_blk + i * 1024);
+    for (int i = 0; i < LOADS; ++i) vx[i] = load_v_stream(vpool + next_blk + i * 1024);
 
     if (nvalid < kPage) {  // ragged last page: padding rows may hold anything
 #pragma unroll
@@ -526,7 +530,30 @@ __device__ void resp_unit(const AttnArgs& a, int item, int h, char* smem) {
         for (int e = 0; e < EPL; ++e) o[r][e] = fmaf(pv, vf[i][e], o[r][e]);
       }
     }
-    page = next_page;
+    pg = next_page;
+  };
+
+  if constexpr (!FP8) {
+    // bf16: one page (8 KiB of K and V at d = 128) in flight per wave.
+    for (int p = wave; p < npages; p += kUnitWaves) step(p, kUnitWaves, page, kr, vr);
+  } else {
+    // fp8 blocks are half the bytes: two pages in flight per wave (register
+    // sets A and B alternate), for the same bytes in flight as bf16 at three
+    // waves per SIMD instead of four.
+    static_assert(kUnitWaves == 1, "two pages in flight per wave");
+    uint4 kb[LOADS], vb[LOADS];
+    int page_b = npages > 1 ? clamp_page(bt[1], a.num_pages) : page;
+    {
+      const size_t blk = resp_block<D, FP8>(a, page_b, h, lane);
+#pragma unroll
+      for (int i = 0; i < LOADS; ++i) kb[i] = *reinterpret_cast<const uint4*>(kpool + blk + i * 1024);
+#pragma unroll
+      for (int i = 0; i < LOADS; ++i) vb[i] = load_v_stream(vpool + blk + i * 1024);
+    }
+    for (int p = 0; p < npages; p += 2) {
+      step(p, 2, page, kr, vr);
+      if (p + 1 < npages) step(p + 1, 2, page_b, kb, vb);
+    }
   }
 
   // Merge the TPL lane groups' states of each wave, then the waves' states
