@@ -533,14 +533,13 @@ __device__ void resp_unit(const AttnArgs& a, int item, int h, char* smem) {
     pg = next_page;
   };
 
-  if constexpr (!FP8) {
-    // bf16: one page (8 KiB of K and V at d = 128) in flight per wave.
+  if constexpr (!FP8 || kUnitWaves > 1) {
+    // One page in flight per wave (bf16: 8 KiB of K and V at d = 128).
     for (int p = wave; p < npages; p += kUnitWaves) step(p, kUnitWaves, page, kr, vr);
   } else {
     // fp8 blocks are half the bytes: two pages in flight per wave (register
     // sets A and B alternate), for the same bytes in flight as bf16 at three
     // waves per SIMD instead of four.
-    static_assert(kUnitWaves == 1, "two pages in flight per wave");
     uint4 kb[LOADS], vb[LOADS];
     int page_b = npages > 1 ? clamp_page(bt[1], a.num_pages) : page;
     {
