@@ -14,8 +14,10 @@
 namespace rp {
 namespace {
 
-constexpr int kPlanThreads = 1024;
-constexpr int kPlanWaves = kPlanThreads / 64;
+// The planner runs as one workgroup: 1024 threads in general, one wave for
+// batches of at most kSmallPlanSeqs sequences (no workgroup barriers to wait
+// on, and a one-wave launch starts sooner).
+constexpr int kSmallPlanSeqs = 64;
 
 __device__ inline long long wave_incl_scan(long long v, int lane) {
 #pragma unroll
@@ -28,7 +30,9 @@ __device__ inline long long wave_incl_scan(long long v, int lane) {
 
 // Exclusive scan across the workgroup; `total` receives the sum. Two packed
 // 32-bit counters add independently as long as neither half overflows.
+template <int kPlanThreads>
 __device__ long long block_excl_scan(long long v, long long* s_tot, long long& total) {
+  constexpr int kPlanWaves = kPlanThreads / 64;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const long long incl = wave_incl_scan(v, lane);
   if (lane == 63) s_tot[wave] = incl;
@@ -56,15 +60,17 @@ __device__ inline long long pack2(int hi, int lo) { return ((long long)hi << 32)
 __device__ inline int hi32(long long v) { return (int)(v >> 32); }
 __device__ inline int lo32(long long v) { return (int)(v & 0xFFFFFFFFll); }
 
-// Sequences planned per pass: their group ids, lengths and piece offsets stay
-// in LDS (a batch with more sequences takes several passes).
-constexpr int kPlanSeqBlock = 4096;
-constexpr int kSeqPerThread = kPlanSeqBlock / kPlanThreads;
 // B-sized pieces written per thread per round.
 constexpr int kItemBatch = 8;
-constexpr int kRoundItems = kItemBatch * kPlanThreads;
 
+// kPlanSeqBlock sequences per pass: their group ids, lengths and piece
+// offsets stay in LDS (a batch with more sequences takes several passes).
+template <int kPlanThreads, int kPlanSeqBlock>
 __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
+  constexpr int kPlanWaves = kPlanThreads / 64;
+  constexpr int kSeqPerThread = kPlanSeqBlock / kPlanThreads;
+  constexpr int kRoundItems = kItemBatch * kPlanThreads;
+  static_assert(kPlanSeqBlock % kPlanThreads == 0, "sequences per thread");
   __shared__ int s_cnt[kPlanMaxGroups];   // members per group, then the group's next member slot
   __shared__ int s_gpc[kPlanMaxGroups];   // prefix chunks per group
   __shared__ int s_sg[kPlanSeqBlock];     // clamped group of each sequence of the pass
@@ -81,7 +87,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
   const PlanView v = a.view;
 
   for (int g = t; g < G; g += kPlanThreads) s_cnt[g] = 0;
-  if (t < kRespChunkPagesMax) s_hist[t] = 0;
+  for (int i = t; i < kRespChunkPagesMax; i += kPlanThreads) s_hist[i] = 0;
   if (t == 0) {
     s_nbig = 0;
     s_pages = 0;
@@ -158,7 +164,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
       npc = cnt > 0 ? s_gpc[g] : 0;
     }
     long long tot;
-    const long long ex = block_excl_scan(pack2(cnt, npc), s_tot, tot);
+    const long long ex = block_excl_scan<kPlanThreads>(pack2(cnt, npc), s_tot, tot);
     if (g < G) {
       const int off = carry_m + hi32(ex);
       v.grp_off[g] = off;
@@ -198,7 +204,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
       sum += cnt[j];
     }
     long long tot;
-    int off = (int)block_excl_scan(sum, s_tot, tot);
+    int off = (int)block_excl_scan<kPlanThreads>(sum, s_tot, tot);
 #pragma unroll
     for (int j = 0; j < kSeqPerThread; ++j) {
       const int k = t * kSeqPerThread + j;
@@ -262,7 +268,8 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
 }  // namespace
 
 hipError_t launch_plan(const PlanArgs& a, hipStream_t stream) {
-  plan_kernel<<<1, kPlanThreads, 0, stream>>>(a);
+  if (a.num_seqs <= kSmallPlanSeqs) plan_kernel<64, 256><<<1, 64, 0, stream>>>(a);
+  else plan_kernel<1024, 4096><<<1, 1024, 0, stream>>>(a);
   return hipGetLastError();
 }
 
