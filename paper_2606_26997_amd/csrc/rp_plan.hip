@@ -14,10 +14,12 @@
 namespace rp {
 namespace {
 
-// The planner runs as one workgroup: 1024 threads in general, one wave for
-// batches of at most kSmallPlanSeqs sequences (no workgroup barriers to wait
-// on, and a one-wave launch starts sooner).
+// The planner runs as one workgroup: 1024 threads in general, four waves for
+// batches of at most kMediumPlanSeqs sequences and one wave for at most
+// kSmallPlanSeqs (fewer waves to meet at each barrier, and a smaller launch
+// starts sooner; measured).
 constexpr int kSmallPlanSeqs = 64;
+constexpr int kMediumPlanSeqs = 256;
 
 __device__ inline long long wave_incl_scan(long long v, int lane) {
 #pragma unroll
@@ -269,6 +271,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
 
 hipError_t launch_plan(const PlanArgs& a, hipStream_t stream) {
   if (a.num_seqs <= kSmallPlanSeqs) plan_kernel<64, 256><<<1, 64, 0, stream>>>(a);
+  else if (a.num_seqs <= kMediumPlanSeqs) plan_kernel<256, 1024><<<1, 256, 0, stream>>>(a);
   else plan_kernel<1024, 4096><<<1, 1024, 0, stream>>>(a);
   return hipGetLastError();
 }
