@@ -304,3 +304,49 @@ def test_frontier_batches_with_longer_pieces(lo, hi, pages):
     ref_out, ref_lse, _ = run_oracle(wl, seqs=seqs)
     compare(out[seqs], lse[seqs], ref_out, ref_lse, "bf16", f"frontier-{pages}")
     assert np.isfinite(out).all() and np.isfinite(lse).all()
+
+
+def _random_case(seed, big=None):
+    """A seeded random batch: head counts, head_dim, kv dtype, group map, lengths and the append all drawn;
+    the response lengths scaled so the pool stays near 150 MB. `big` = (kv dtype, sequences, longest
+    response) fixes Hkv 8, d 64 and enough response pages for 64- or 96-page pieces on a 256-CU GPU."""
+    rng = np.random.default_rng(seed)
+    Hkv = int(rng.choice([1, 2, 4, 8]))
+    nrep = int(rng.choice([1, 2, 4, 8] if Hkv <= 4 else [1, 2, 4]))
+    d = int(rng.choice([64, 128]))
+    dt = str(rng.choice(["bf16", "fp8"]))
+    S = int(rng.integers(4, 260))
+    if big is not None:
+        Hkv, d, (dt, S, _) = 8, 64, big
+    G = int(rng.integers(1, S + 1))
+    s2g = rng.integers(0, G, S)
+    P = rng.integers(0, 700, G)
+    per_token = Hkv * d * 2 * (1 if dt == "fp8" else 2)
+    Lmax = int(max(16, min(20000, 150e6 / per_token / S * 2))) if big is None else big[2]
+    L = rng.integers(0, Lmax + 1, S)
+    return dict(num_q_heads=Hkv * nrep, num_kv_heads=Hkv, head_dim=d, seq_to_group=s2g, prefix_lens=P,
+                resp_lens=L, seed=seed, kv_dtype=dt, append=bool(rng.integers(0, 2)))
+
+
+RANDOM = [(11, None), (22, None), (33, None), (44, None), (55, None), (66, None),
+          (77, ("fp8", 120, 4500)), (88, ("bf16", 64, 5000))]
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("seed,big", RANDOM, ids=[str(r[0]) for r in RANDOM])
+def test_random_batches_sampled_rows(seed, big):
+    """Random shapes across the kernel templates (n_rep, head_dim, kv dtype) and piece lengths; the
+    oracle runs on sampled sequences (longest, shortest and six random)."""
+    kw = _random_case(seed, big)
+    wl = make_workload(**kw)
+    _say(f"random seed {seed}: S {wl.num_seqs}, G {wl.num_groups}, Hq {wl.num_q_heads}, Hkv {wl.num_kv_heads}, "
+         f"d {wl.head_dim}, {wl.kv_dtype}, append {wl.append}, pages {wl.num_pages}")
+    batch, out, lse = run_hip(wl)
+    _say(f"random seed {seed}: piece length {int(batch.plan_contents()['hdr'][3])} pages")
+    rng = np.random.default_rng(seed + 1)
+    L = wl.attn_resp_lens
+    S = wl.num_seqs
+    seqs = sorted({int(np.argmax(L)), int(np.argmin(L))} | set(rng.choice(S, size=min(6, S), replace=False).tolist()))
+    ref_out, ref_lse, _ = run_oracle(wl, seqs=seqs)
+    compare(out[seqs], lse[seqs], ref_out, ref_lse, wl.kv_dtype, f"random-{seed}")
+    assert np.isfinite(out[np.isfinite(lse)]).all()
