@@ -108,9 +108,9 @@ __global__ __launch_bounds__(64) void prefill_kv_write_kernel(const PrefillArgs 
 // wave w holds RT 16-row tiles (each 16 / n_rep consecutive prompt tokens
 // times the n_rep query heads of the kv-head), so a workgroup covers
 // 64 RT / n_rep tokens. Keys go through LDS in blocks of 32, double-buffered:
-// while the waves compute on one block, the next block's K (row-major) and V
-// (transposed, so that an MFMA operand of V^T is one 8-byte read) are loaded
-// from the projections and written into the other buffer; one barrier per
+// while the waves compute on one block, the next block's K and V (both
+// row-major, as in the projections) are loaded from the projections and
+// written into the other buffer; one barrier per
 // block. Per block and row tile: S^T = K Q^T on mfma 16x16x32 (Q stays in
 // registers), a causal mask, one online-softmax update per row, and
 // O^T += V^T P^T, also on mfma 16x16x32 (all 32 keys per instruction).
@@ -118,18 +118,24 @@ constexpr int kPfWaves = 4;
 constexpr int kPfThreads = 64 * kPfWaves;
 constexpr int kKeyBlk = 32;
 
+// Both K and V are staged row-major, as they come from the projections. The
+// V^T operand of P V is read with gfx950's transposing LDS read
+// (ds_read_b64_tr_b16): within each 16-lane group, lane s supplies the
+// address of 4 consecutive 16-bit elements, and lane j receives element j % 4
+// of the elements addressed by lanes j / 4, 4 + j / 4, 8 + j / 4 and
+// 12 + j / 4, in that order. With lane s pointing at row r0 + s / 4, columns
+// c0 + 4 (s % 4) ... + 3, lane j receives rows r0 .. r0 + 3 of column c0 + j.
 template <int D>
 struct PfSmem {
-  static constexpr int kKPitch = D + 8;        // K rows, bf16 (16-byte aligned rows)
-  static constexpr int kVPitch = kKeyBlk + 4;  // V^T rows, bf16
+  static constexpr int kKPitch = D + 8;   // K rows, bf16 (16-byte aligned rows)
+  static constexpr int kVPitch = D + 16;  // V rows, bf16: 4 consecutive rows start 8 banks apart
   static constexpr int kKElems = kKeyBlk * kKPitch;
-  static constexpr int kStage = kKElems + D * kVPitch;
+  static constexpr int kStage = kKElems + kKeyBlk * kVPitch;
   static constexpr int kBytes = 2 * kStage * 2;
-  static constexpr int kKChunks = kKeyBlk * D / 8;          // 16-byte pieces of a K block
-  static constexpr int kVChunks = (kKeyBlk / 2) * (D / 8);  // (2 keys x 8 columns) pieces of a V block
-  static constexpr int kKPerThread = kKChunks / kPfThreads;
-  static_assert(kKChunks % kPfThreads == 0, "K block split");
-  static_assert(kVChunks <= kPfThreads, "V block split");
+  static constexpr int kChunks = kKeyBlk * D / 8;  // 16-byte pieces of a K (or V) block
+  static constexpr int kPerThread = kChunks / kPfThreads;
+  static_assert(kChunks % kPfThreads == 0, "block split");
+  static_assert(kPerThread == 1 || kPerThread == 2, "pieces per thread");
 };
 
 // This thread's share of one key block, in registers between the global
@@ -146,48 +152,43 @@ template <int D>
 __device__ inline void pf_load(const uint16_t* kbase, const uint16_t* vbase, size_t pitch, int u0, int last, int t,
                                PfBlock& r) {
   using L = PfSmem<D>;
-  static_assert(L::kKPerThread == 1 || L::kKPerThread == 2, "K pieces per thread");
   {
     const int key = t / (D / 8), col = (t - key * (D / 8)) * 8;
-    r.k0 = *reinterpret_cast<const u32x4_t*>(kbase + (size_t)min(u0 + key, last) * pitch + col);
+    const size_t off = (size_t)min(u0 + key, last) * pitch + col;
+    r.k0 = *reinterpret_cast<const u32x4_t*>(kbase + off);
+    r.v0 = *reinterpret_cast<const u32x4_t*>(vbase + off);
   }
-  if constexpr (L::kKPerThread == 2) {
+  if constexpr (L::kPerThread == 2) {
     const int c = t + kPfThreads;
     const int key = c / (D / 8), col = (c - key * (D / 8)) * 8;
-    r.k1 = *reinterpret_cast<const u32x4_t*>(kbase + (size_t)min(u0 + key, last) * pitch + col);
-  }
-  if (L::kVChunks == kPfThreads || t < L::kVChunks) {
-    const int kp = t % (kKeyBlk / 2), d0 = (t / (kKeyBlk / 2)) * 8;
-    r.v0 = *reinterpret_cast<const u32x4_t*>(vbase + (size_t)min(u0 + 2 * kp, last) * pitch + d0);
-    r.v1 = *reinterpret_cast<const u32x4_t*>(vbase + (size_t)min(u0 + 2 * kp + 1, last) * pitch + d0);
+    const size_t off = (size_t)min(u0 + key, last) * pitch + col;
+    r.k1 = *reinterpret_cast<const u32x4_t*>(kbase + off);
+    r.v1 = *reinterpret_cast<const u32x4_t*>(vbase + off);
   }
 }
 
 template <int D>
 __device__ inline void pf_store(uint16_t* stage, int t, const PfBlock& r) {
   using L = PfSmem<D>;
+  uint16_t* vst = stage + L::kKElems;
   {
     const int key = t / (D / 8), col = (t - key * (D / 8)) * 8;
     *reinterpret_cast<u32x4_t*>(stage + key * L::kKPitch + col) = r.k0;
+    *reinterpret_cast<u32x4_t*>(vst + key * L::kVPitch + col) = r.v0;
   }
-  if constexpr (L::kKPerThread == 2) {
+  if constexpr (L::kPerThread == 2) {
     const int c = t + kPfThreads;
     const int key = c / (D / 8), col = (c - key * (D / 8)) * 8;
     *reinterpret_cast<u32x4_t*>(stage + key * L::kKPitch + col) = r.k1;
+    *reinterpret_cast<u32x4_t*>(vst + key * L::kVPitch + col) = r.v1;
   }
-  if (L::kVChunks == kPfThreads || t < L::kVChunks) {
-    const int kp = t % (kKeyBlk / 2), d0 = (t / (kKeyBlk / 2)) * 8;
-    uint16_t* vt = stage + L::kKElems + d0 * L::kVPitch + 2 * kp;
-    // Columns d0 + 2e and d0 + 2e + 1 of keys 2kp (low halves) and 2kp + 1 (high halves).
-    const auto put = [&](int e, uint32_t a, uint32_t b) {
-      *reinterpret_cast<uint32_t*>(vt + (2 * e) * L::kVPitch) = (a & 0xFFFFu) | (b << 16);
-      *reinterpret_cast<uint32_t*>(vt + (2 * e + 1) * L::kVPitch) = (a >> 16) | (b & 0xFFFF0000u);
-    };
-    put(0, r.v0.x, r.v1.x);
-    put(1, r.v0.y, r.v1.y);
-    put(2, r.v0.z, r.v1.z);
-    put(3, r.v0.w, r.v1.w);
-  }
+}
+
+// Four keys of one V column from the row-major staged block (see PfSmem).
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+__device__ inline bf16x4_t lds_read_tr(const uint16_t* p) {
+  return __builtin_bit_cast(
+      bf16x4_t, __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4_t*)(p)));
 }
 
 // One 32-key block from LDS stage `kst` (keys u0 .. u0 + 31) for this wave's
@@ -220,11 +221,11 @@ __device__ __forceinline__ void pf_compute(const uint16_t* kst, int u0, int last
   }
   // V^T operands of the whole block, read while the softmax runs.
   bf16x8_t vop[DT];
+  const uint16_t* vtr = vst + (quad * 4 + r16 / 4) * L::kVPitch + 4 * (r16 % 4);
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt) {
-    const uint16_t* vrow = vst + (dt * 16 + r16) * L::kVPitch + quad * 4;
-    const bf16x4_t v0 = __builtin_bit_cast(bf16x4_t, *reinterpret_cast<const uint2*>(vrow));
-    const bf16x4_t v1 = __builtin_bit_cast(bf16x4_t, *reinterpret_cast<const uint2*>(vrow + 16));
+    const bf16x4_t v0 = lds_read_tr(vtr + dt * 16);
+    const bf16x4_t v1 = lds_read_tr(vtr + 16 * L::kVPitch + dt * 16);
     vop[dt] = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
   }
   bf16x4_t pop[RT][ST];
@@ -274,6 +275,9 @@ __device__ __forceinline__ void pf_compute(const uint16_t* kst, int u0, int last
   // columns: lane (r16, quad) supplies contraction slots 8 quad .. 8 quad + 7,
   // taken as keys quad*4 .. quad*4 + 3 and 16 + quad*4 .. 16 + quad*4 + 3 in
   // both operands (any key order serves, as long as V^T and P^T share it).
+  // The V^T operand of lane (r16, quad) is column dt*16 + r16 of those keys:
+  // two transposing reads, in which lane s of the quad's 16 points at row
+  // quad*4 + s/4 (then 16 rows further on), columns dt*16 + 4 (s % 4) ...+3.
   static_assert(ST == 2, "two 16-key sub-tiles per block");
   bf16x8_t pop8[RT];
 #pragma unroll
