@@ -1,6 +1,7 @@
 // C-ABI entry points: argument validation, workspace layout and kernel
 // launches on the caller's stream. No device allocation and no host sync on
 // the hot path; rp_validate_layout is the one test utility that does both.
+#include <atomic>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -133,20 +134,20 @@ bool ws_layout(const Shape& sh, WsLayout* w) {
 }
 
 // Compute units of the current device, queried once per device (racing first
-// calls store the same value).
+// calls store the same value; relaxed atomics keep that race defined).
 rp_status device_cus(int* cus) {
-  static int cache[64] = {0};
+  static std::atomic<int> cache[64];
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
   if (dev < 0 || dev >= 64) return fail(RP_ERR_UNSUPPORTED, "device %d out of range", dev);
-  if (cache[dev] == 0) {
-    int n = 0;
+  int n = cache[dev].load(std::memory_order_relaxed);
+  if (n == 0) {
     e = hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev);
     if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute");
-    cache[dev] = n;
+    cache[dev].store(n, std::memory_order_relaxed);
   }
-  *cus = cache[dev];
+  *cus = n;
   return RP_OK;
 }
 
