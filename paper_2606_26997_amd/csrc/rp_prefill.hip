@@ -219,21 +219,15 @@ __device__ __forceinline__ void pf_compute(const uint16_t* kst, int u0, int last
       for (int rt = 0; rt < RT; ++rt) sacc[rt][st] = mfma16x16x32(kop, qop[rt][kb], sacc[rt][st]);
     }
   }
-  // V^T operands of the whole block, read while the softmax runs (two row
-  // tiles per wave), or one at a time inside P V (one row tile per wave:
-  // fewer live registers keep four waves per SIMD).
-  constexpr bool kVAhead = RT >= 2;
-  bf16x8_t vop[kVAhead ? DT : 1];
+  // V^T operands are read inside P V, one 16-column tile at a time: fewer
+  // live registers than reading the whole block's ahead of the softmax,
+  // which keeps four waves per SIMD with one row tile and three with two.
   const uint16_t* vtr = vst + (quad * 4 + r16 / 4) * L::kVPitch + 4 * (r16 % 4);
   const auto read_vop = [&](int dt) __attribute__((always_inline)) {
     const bf16x4_t v0 = lds_read_tr(vtr + dt * 16);
     const bf16x4_t v1 = lds_read_tr(vtr + 16 * L::kVPitch + dt * 16);
     return __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
   };
-  if constexpr (kVAhead) {
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt) vop[dt] = read_vop(dt);
-  }
   bf16x4_t pop[RT][ST];
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt) {
@@ -291,16 +285,16 @@ __device__ __forceinline__ void pf_compute(const uint16_t* kst, int u0, int last
     pop8[rt] = __builtin_shufflevector(pop[rt][0], pop[rt][1], 0, 1, 2, 3, 4, 5, 6, 7);
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt) {
-    const bf16x8_t vo = kVAhead ? vop[kVAhead ? dt : 0] : read_vop(dt);
+    const bf16x8_t vo = read_vop(dt);
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) oacc[rt][dt] = mfma16x16x32(vo, pop8[rt], oacc[rt][dt]);
   }
 }
 
 // Register budget: one row tile per wave fits four waves per SIMD (128
-// VGPRs, V^T operands read inside P V); two row tiles take two.
+// VGPRs), two row tiles three (168 VGPRs).
 template <int D, int NREP, int RT>
-__global__ __launch_bounds__(kPfThreads) __attribute__((amdgpu_waves_per_eu(RT == 1 ? 4 : 2, 8)))
+__global__ __launch_bounds__(kPfThreads) __attribute__((amdgpu_waves_per_eu(RT == 1 ? 4 : 3, 8)))
 void prefill_attn_kernel(const PrefillArgs a, int max_blocks) {
   using L = PfSmem<D>;
   constexpr int KB = D / 32;              // MFMA k-blocks over head_dim
