@@ -263,20 +263,23 @@ def prefill_bench(args):
         nbytes += int(((P64 + 15) // 16).sum()) * Hkv * 8
     # Causal attention flops: QK and PV over the u <= t pairs (2 flops per multiply-add).
     flops = int((P64 * (P64 + 1) // 2).sum()) * Hq * d * 4
+    # One step is rp_prefill: for a bf16 pool a single launch of the attention
+    # kernel that also writes the pages; for fp8 the page-write kernel first.
     for _ in range(args.warmup):
-        b.step()
+        b.prefill()
     torch.cuda.synchronize()
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
     t0 = time.perf_counter()
     for k in range(args.steps):
-        b.kv_write()
         ev[k][0].record()
-        b.attention()
+        b.prefill()
         ev[k][1].record()
     torch.cuda.synchronize()
     ms = (time.perf_counter() - t0) / args.steps * 1e3
     attn_us = float(np.mean([a.elapsed_time(c) for a, c in ev])) * 1e3
-    attn_bytes = T * (Hq + 2 * Hkv + Hq) * d * 2 + T * Hq * 4
+    # The timed launch's bytes: q, k, v read, out and lse written, and (bf16,
+    # one launch) the pages written.
+    attn_bytes = T * (Hq + 2 * Hkv + Hq) * d * 2 + T * Hq * 4 + (T * Hkv * d * 2 * eb if eb == 2 else 0)
     # Below the bf16 ridge (about 310 flop/B) the kernel is priced against HBM
     # bandwidth, above it against the dense bf16 MFMA peak.
     gbps_attn = attn_bytes / (attn_us * 1e-6) / 1e9

@@ -221,6 +221,17 @@ rp_status rp_prefill_attn(const rp_paged_kv* kv, const rp_prefill_layout* layout
                           const void* q, const void* k, const void* v, float softmax_scale,
                           void* out, float* lse, hipStream_t stream);
 
+/* The whole prefill of a step: rp_prefill_kv_write and rp_prefill_attn with
+ * the same arguments, in that order, with the same results (the same page
+ * bytes, out and lse). For a bf16 pool it is one launch: the attention
+ * kernel stages every prompt's K/V blocks anyway, and the workgroup whose
+ * query rows start a block also copies it into the pages. An fp8 pool takes
+ * the page-write kernel first, because each page's scale needs the whole
+ * page. Same argument rules and errors as the two calls. */
+rp_status rp_prefill(const rp_paged_kv* kv, const rp_prefill_layout* layout,
+                     const void* q, const void* k, const void* v, float softmax_scale,
+                     void* out, float* lse, hipStream_t stream);
+
 /* ---- Staged form of rp_group_decode_attn -------------------------------
  * A decode step's layout is shared by every layer, so a caller can plan once
  * and run the attention of all layers against the same plan. */

@@ -10,7 +10,7 @@ from ._binding import (EXPORTED, LIB_PATH, RP_ERR_HIP, RP_ERR_INVALID_ARG, RP_ER
                        RpError, RpGroupLayout, RpPagedKV, RpPrefillLayout, combine_parts,
                        decode_qk_prep, grpo_advantage, group_decode_attn, group_decode_attn_workspace_size, group_layout,
                        kv_append, last_error, load, lse_combine, paged_kv, plan, attn_parts,
-                       prefill_attn, prefill_kv_write, prefill_layout, status_string,
+                       prefill, prefill_attn, prefill_kv_write, prefill_layout, status_string,
                        sched_simulate, validate_layout)
 from .batch import DeviceBatch, PrefillBatch
 
@@ -19,5 +19,5 @@ __all__ = ["EXPORTED", "LIB_PATH", "RP_OK", "RP_ERR_INVALID_ARG", "RP_ERR_UNSUPP
            "RpError", "RpPagedKV", "RpGroupLayout", "load", "status_string", "last_error",
            "paged_kv", "group_layout", "kv_append", "group_decode_attn_workspace_size",
            "group_decode_attn", "lse_combine", "plan", "attn_parts", "combine_parts",
-           "validate_layout", "DeviceBatch", "RpPrefillLayout", "prefill_layout", "prefill_kv_write",
+           "validate_layout", "DeviceBatch", "RpPrefillLayout", "prefill_layout", "prefill_kv_write", "prefill",
            "prefill_attn", "PrefillBatch", "decode_qk_prep", "sched_simulate", "grpo_advantage"]

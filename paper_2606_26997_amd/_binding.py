@@ -29,7 +29,7 @@ EXPORTED = ("rp_status_string", "rp_last_error", "rp_kv_append",
             "rp_group_decode_attn_workspace_size", "rp_group_decode_attn", "rp_lse_combine",
             "rp_plan", "rp_attn_parts", "rp_combine_parts", "rp_plan_layout", "rp_validate_layout",
             "rp_prefill_kv_write", "rp_prefill_attn", "rp_decode_qk_prep", "rp_sched_simulate",
-            "rp_grpo_advantage")
+            "rp_grpo_advantage", "rp_prefill")
 RP_SCHED_MODES = {"slime": 0, "cgp": 1, "cgp_fgd": 2}
 
 
@@ -109,6 +109,7 @@ def load() -> ctypes.CDLL:
         "rp_validate_layout": (ctypes.c_int, [P, P, P]),
         "rp_prefill_kv_write": (ctypes.c_int, [P, P, P, P, P]),
         "rp_prefill_attn": (ctypes.c_int, [P, P, P, P, P, F32, P, P, P]),
+        "rp_prefill": (ctypes.c_int, [P, P, P, P, P, F32, P, P, P]),
         "rp_decode_qk_prep": (ctypes.c_int, [P, P, P, P, P, P, P, ctypes.c_double, ctypes.c_double, P, P, P]),
         "rp_sched_simulate": (ctypes.c_int, [P, P, P, P, P, P, P, P, P, P]),
         "rp_grpo_advantage": (ctypes.c_int, [P, I32, I32, ctypes.c_double, I32, P, P, P, P]),
@@ -264,6 +265,11 @@ def prefill_kv_write(kv, layout, k, v, stream=None) -> None:
 def prefill_attn(kv, layout, q, k, v, softmax_scale, out, lse, stream=None) -> None:
     _check(load().rp_prefill_attn(ctypes.byref(kv), ctypes.byref(layout), _ptr(q), _ptr(k), _ptr(v),
                                   float(softmax_scale), _ptr(out), _ptr(lse), _stream(stream)), "rp_prefill_attn")
+
+
+def prefill(kv, layout, q, k, v, softmax_scale, out, lse, stream=None) -> None:
+    _check(load().rp_prefill(ctypes.byref(kv), ctypes.byref(layout), _ptr(q), _ptr(k), _ptr(v),
+                             float(softmax_scale), _ptr(out), _ptr(lse), _stream(stream)), "rp_prefill")
 
 
 def sched_simulate(*, mode, group_size, update_groups, prompt_lens, resp_lens, max_running, frontier_width=0,

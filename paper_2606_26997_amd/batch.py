@@ -181,6 +181,10 @@ class PrefillBatch:
         B.prefill_attn(self.kv, self.layout, self.q, self.k, self.v, self.softmax_scale, self.out, self.lse, stream)
 
     def step(self, stream=None):
-        """Write the prompts' K/V pages, then attend within each prompt."""
+        """Write the prompts' K/V pages, then attend within each prompt (two calls)."""
         self.kv_write(stream)
         self.attention(stream)
+
+    def prefill(self, stream=None):
+        """The same results as ``step`` through rp_prefill (one launch for a bf16 pool)."""
+        B.prefill(self.kv, self.layout, self.q, self.k, self.v, self.softmax_scale, self.out, self.lse, stream)

@@ -500,8 +500,12 @@ rp_status rp_prefill_kv_write(const rp_paged_kv* kv, const rp_prefill_layout* l,
   return e == hipSuccess ? RP_OK : hip_fail(e, "prefill KV write kernel launch");
 }
 
-rp_status rp_prefill_attn(const rp_paged_kv* kv, const rp_prefill_layout* l, const void* q, const void* k,
-                          const void* v, float softmax_scale, void* out, float* lse, hipStream_t stream) {
+// Causal attention within each prompt; with `pages`, also the prompts' K/V
+// page writes: in the same launch for bf16 pools, by the page-write kernel
+// first for fp8 pools (their per-page scales need a whole page).
+static rp_status prefill_impl(const rp_paged_kv* kv, const rp_prefill_layout* l, const void* q, const void* k,
+                              const void* v, float softmax_scale, void* out, float* lse, bool pages,
+                              hipStream_t stream) {
   g_err[0] = 0;
   rp::PrefillArgs a{};
   int n_rep = 0;
@@ -520,8 +524,24 @@ rp_status rp_prefill_attn(const rp_paged_kv* kv, const rp_prefill_layout* l, con
   a.qk_scale = softmax_scale * rp::kLog2e;
   a.out = out;
   a.lse = lse;
+  const bool fp8 = kv->kv_dtype == RP_KV_FP8_E4M3;
+  if (pages && fp8) {
+    hipError_t e = rp::launch_prefill_kv_write(a, kv->head_dim, true, stream);
+    if (e != hipSuccess) return hip_fail(e, "prefill KV write kernel launch");
+  }
+  a.write_pages = pages && !fp8 ? 1 : 0;
   hipError_t e = rp::launch_prefill_attn(a, kv->head_dim, n_rep, stream);
   return e == hipSuccess ? RP_OK : hip_fail(e, "prefill attention kernel launch");
+}
+
+rp_status rp_prefill_attn(const rp_paged_kv* kv, const rp_prefill_layout* l, const void* q, const void* k,
+                          const void* v, float softmax_scale, void* out, float* lse, hipStream_t stream) {
+  return prefill_impl(kv, l, q, k, v, softmax_scale, out, lse, false, stream);
+}
+
+rp_status rp_prefill(const rp_paged_kv* kv, const rp_prefill_layout* l, const void* q, const void* k, const void* v,
+                     float softmax_scale, void* out, float* lse, hipStream_t stream) {
+  return prefill_impl(kv, l, q, k, v, softmax_scale, out, lse, true, stream);
 }
 
 rp_status rp_plan_layout(const rp_paged_kv* kv, const rp_group_layout* l, rp_plan_info* info) {

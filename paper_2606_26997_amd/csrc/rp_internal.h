@@ -135,6 +135,7 @@ struct PrefillArgs {
   float qk_scale;  // softmax_scale * log2(e)
   void* out;       // bf16 [T][Hq][D]
   float* lse;      // [T][Hq] or null
+  int write_pages;  // attention kernel also writes the bf16 K/V pages (one launch for the whole prefill)
 };
 
 struct ValidateArgs {

@@ -184,6 +184,29 @@ __device__ inline void pf_store(uint16_t* stage, int t, const PfBlock& r) {
   }
 }
 
+// The one-launch prefill of a bf16 pool: the workgroup whose query rows
+// include a key block's first token copies that block's staged K/V rows (the
+// thread's registers, after they went to LDS) into the group's prefix pages.
+// Rows past the prompt's end are not written, as in the page-write kernel.
+template <int D>
+__device__ inline void pf_write_pages(const PrefillArgs& a, int g, int h, int u0, int last, int t,
+                                      const PfBlock& r) {
+  using L = PfSmem<D>;
+  const int* pbt = a.prefix_block_table + (size_t)g * a.max_prefix_pages;
+  uint16_t* kp = static_cast<uint16_t*>(a.k_pages);
+  uint16_t* vp = static_cast<uint16_t*>(a.v_pages);
+  const auto put = [&](int c, const u32x4_t& kk, const u32x4_t& vv) __attribute__((always_inline)) {
+    const int key = c / (D / 8), col = (c - key * (D / 8)) * 8, u = u0 + key;
+    if (u > last) return;
+    const int page = clamp_page(pbt[u / kPage], a.num_pages);
+    const size_t off = (((size_t)page * a.num_kv_heads + h) * kPage + (u % kPage)) * D + col;
+    *reinterpret_cast<u32x4_t*>(kp + off) = kk;
+    *reinterpret_cast<u32x4_t*>(vp + off) = vv;
+  };
+  put(t, r.k0, r.v0);
+  if constexpr (L::kPerThread == 2) put(t + kPfThreads, r.k1, r.v1);
+}
+
 // Four keys of one V column from the row-major staged block (see PfSmem).
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
 __device__ inline bf16x4_t lds_read_tr(const uint16_t* p) {
@@ -293,8 +316,8 @@ __device__ __forceinline__ void pf_compute(const uint16_t* kst, int u0, int last
 
 // Register budget: one row tile per wave fits four waves per SIMD (128
 // VGPRs), two row tiles three (168 VGPRs).
-template <int D, int NREP, int RT>
-__global__ __launch_bounds__(kPfThreads) __attribute__((amdgpu_waves_per_eu(RT == 1 ? 4 : 3, 8)))
+template <int D, int NREP, int RT, bool WP>
+__global__ __launch_bounds__(kPfThreads) __attribute__((amdgpu_waves_per_eu(RT == 1 ? (WP ? 3 : 4) : (WP ? 2 : 3), 8)))
 void prefill_attn_kernel(const PrefillArgs a, int max_blocks) {
   using L = PfSmem<D>;
   constexpr int KB = D / 32;              // MFMA k-blocks over head_dim
@@ -350,9 +373,12 @@ void prefill_attn_kernel(const PrefillArgs a, int max_blocks) {
   // The next block's loads are issued before this block's compute and
   // written to the other LDS buffer after it (past the last block they read
   // clamped rows and are never used).
+  // With write_pages, key block b's rows go to the pages from the workgroup
+  // whose rows hold token 32 b (every block of the prompt has exactly one).
   PfBlock nx;
   pf_load<D>(kbase, vbase, kpitch, 0, last, t, nx);
   pf_store<D>(smem, t, nx);
+  if (WP && T0 == 0) pf_write_pages<D>(a, g, h, 0, last, t, nx);
   __syncthreads();
   for (int blk = 0; blk < nblk; ++blk) {
     pf_load<D>(kbase, vbase, kpitch, (blk + 1) * kKeyBlk, last, t, nx);
@@ -364,6 +390,8 @@ void prefill_attn_kernel(const PrefillArgs a, int max_blocks) {
       pf_compute<D, NREP, RT, true>(smem + (blk & 1) * L::kStage, blk * kKeyBlk, last, a.qk_scale, r16, quad, tr,
                                     qop, oacc, mrow, lrow);
     pf_store<D>(smem + ((blk + 1) & 1) * L::kStage, t, nx);
+    const int un = (blk + 1) * kKeyBlk;
+    if (WP && un >= T0 && un < T0 + TPB) pf_write_pages<D>(a, g, h, un, last, t, nx);
     __syncthreads();  // the next block is staged; this block's buffer may be overwritten next
   }
 
@@ -395,8 +423,13 @@ hipError_t attn_launch(const PrefillArgs& a, hipStream_t st) {
   const long long blocks = NP * max_blocks;
   if (blocks <= 0) return hipSuccess;
   const dim3 grid((unsigned)blocks), block(kPfThreads);
-  if (rt == 2) prefill_attn_kernel<D, NREP, 2><<<grid, block, 0, st>>>(a, max_blocks);
-  else prefill_attn_kernel<D, NREP, 1><<<grid, block, 0, st>>>(a, max_blocks);
+  if (a.write_pages) {
+    if (rt == 2) prefill_attn_kernel<D, NREP, 2, true><<<grid, block, 0, st>>>(a, max_blocks);
+    else prefill_attn_kernel<D, NREP, 1, true><<<grid, block, 0, st>>>(a, max_blocks);
+  } else {
+    if (rt == 2) prefill_attn_kernel<D, NREP, 2, false><<<grid, block, 0, st>>>(a, max_blocks);
+    else prefill_attn_kernel<D, NREP, 1, false><<<grid, block, 0, st>>>(a, max_blocks);
+  }
   return hipGetLastError();
 }
 

@@ -138,3 +138,26 @@ def test_decode_over_prefilled_pages_matches_last_prompt_row():
     assert np.abs(o_dec - o_pre).max() <= 1e-2
     np.testing.assert_allclose(dec.lse.cpu().numpy(), b.lse[torch.as_tensor(last, device=dev)].cpu().numpy(),
                                rtol=0, atol=1e-4)
+
+
+@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
+def test_one_call_prefill_matches_the_two_calls(case):
+    """rp_prefill (one launch for bf16 pools: the attention kernel also writes the pages) gives the same page
+    bytes, scales, out and lse as rp_prefill_kv_write then rp_prefill_attn, and matches the oracle."""
+    import paper_2606_26997_amd as rp
+    name, P, Hq, Hkv, d, dt = case
+    _say(f"one-call prefill {name}")
+    w = make_prefill_workload(num_q_heads=Hq, num_kv_heads=Hkv, head_dim=d, prefix_lens=P, seed=len(name),
+                              kv_dtype=dt)
+    two = _run(w)
+    one = rp.PrefillBatch.from_workload(w)
+    one.prefill()
+    torch.cuda.synchronize()
+    assert torch.equal(one.k_pages.view(torch.uint8), two.k_pages.view(torch.uint8)), name
+    assert torch.equal(one.v_pages.view(torch.uint8), two.v_pages.view(torch.uint8)), name
+    if dt == "fp8":
+        assert torch.equal(one.k_scale, two.k_scale) and torch.equal(one.v_scale, two.v_scale), name
+    assert torch.equal(one.out.view(torch.int16), two.out.view(torch.int16)), name
+    assert torch.equal(one.lse.view(torch.int32), two.lse.view(torch.int32)), name
+    _check_pages(one, w, name)
+    _check_attn(one, w, name)
