@@ -21,7 +21,8 @@ def bf16_to_f64(bits) -> np.ndarray:
         return bf16_to_f32(bits).astype(np.float64)
 
 
-def e4m3_to_f64(codes) -> np.ndarray:
+def _e4m3_decode_definition(codes) -> np.ndarray:
+    """e4m3fn code -> value, straight from the bit fields (sign, exponent, mantissa)."""
     c = np.asarray(codes, dtype=np.uint8).astype(np.int64)
     sign = (c >> 7) & 1
     e = (c >> 3) & 0xF
@@ -29,6 +30,15 @@ def e4m3_to_f64(codes) -> np.ndarray:
     mag = np.where(e == 0, m * 2.0 ** -9, (1.0 + m / 8.0) * np.exp2(e - 7.0))
     mag = np.where((e == 15) & (m == 7), np.nan, mag)
     return np.where(sign == 1, -mag, mag)
+
+
+# The definition evaluated once for each of the 256 codes; decoding a pool is
+# then a lookup (the same values, without the per-element field arithmetic).
+_E4M3_VALUES = _e4m3_decode_definition(np.arange(256, dtype=np.uint8))
+
+
+def e4m3_to_f64(codes) -> np.ndarray:
+    return _E4M3_VALUES[np.asarray(codes, dtype=np.uint8)]
 
 
 # Magnitudes of the 127 non-negative finite codes 0x00..0x7E, increasing with the code.

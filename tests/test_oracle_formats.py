@@ -72,3 +72,14 @@ def test_e4m3_roundtrip_error_within_half_ulp():
     e = np.floor(np.log2(np.maximum(a, 2.0 ** -6)))
     ulp = 2.0 ** (e - 3)
     assert np.all(np.abs(y - x) <= ulp / 2)
+
+
+def test_e4m3_lookup_equals_the_bit_field_definition_on_pool_shapes():
+    """The decode table is the bit-field definition evaluated per code: same values on any array."""
+    from oracle.formats import _e4m3_decode_definition
+    codes = np.random.default_rng(5).integers(0, 256, (3, 2, 16, 8)).astype(np.uint8)
+    a, b = e4m3_to_f64(codes), _e4m3_decode_definition(codes)
+    assert a.shape == codes.shape and a.dtype == np.float64
+    nan = np.isnan(b)
+    assert np.array_equal(np.isnan(a), nan) and np.array_equal(a[~nan], b[~nan])
+    assert np.array_equal(np.signbit(a[~nan]), np.signbit(b[~nan]))
