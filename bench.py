@@ -37,9 +37,12 @@ if ROOT not in sys.path:
 
 METRIC = "decode-attn achieved HBM GB/s (% of MI355X peak) + seq-steps/s per layer"
 HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E, vendor figure
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_attn_parts_config2.json")
-KERNEL_SOURCES = ["paper_2606_26997_amd/csrc/rp_attn.hip", "paper_2606_26997_amd/csrc/rp_device.h",
-                  "paper_2606_26997_amd/csrc/rp_internal.h"]
+# Stored HBM counter summaries of the partial-attention kernel, one file per workload.
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_attn_parts_{workload}.json")
+# What the partial-attention kernel is built from: its source, the device helpers it includes and
+# its argument structs (the counters stay valid while none of these change).
+KERNEL_SOURCES = ["paper_2606_26997_amd/csrc/rp_attn.hip", "paper_2606_26997_amd/csrc/rp_device.h"]
+KERNEL_STRUCTS = ("paper_2606_26997_amd/csrc/rp_internal.h", "struct AttnArgs {")
 
 
 def parse_args():
@@ -47,7 +50,8 @@ def parse_args():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=100)
     p.add_argument("--warmup", type=int, default=10)
-    p.add_argument("--config", type=int, default=2, help="workload number 1-5 (default 2)")
+    p.add_argument("--config", type=int, default=None,
+                   help="workload number 1-5 (default: configs 3, 4, 5 on stderr, then config 2, the headline)")
     p.add_argument("--seed", type=int, default=None)
     p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="wall-clock budget of the oracle CPU baseline sample (0 disables it)")
@@ -79,6 +83,10 @@ def kernel_source_hash():
     for rel in KERNEL_SOURCES:
         with open(os.path.join(ROOT, rel), "rb") as f:
             h.update(f.read())
+    path, head = KERNEL_STRUCTS
+    text = open(os.path.join(ROOT, path)).read()
+    i = text.index(head)
+    h.update(text[i:text.index("};", i) + 2].encode())
     return h.hexdigest()[:16]
 
 
@@ -120,47 +128,95 @@ def byte_model(wl):
 def load_traffic(workload):
     """HBM traffic of the partial-attention kernel from stored rocprofv3 counter runs, if they
     were taken on this workload with the current kernel sources."""
-    if not os.path.exists(TRAFFIC_FILE):
+    path = TRAFFIC_FILE.format(workload=workload)
+    if not os.path.exists(path):
         return None
-    with open(TRAFFIC_FILE) as f:
+    with open(path) as f:
         t = json.load(f)
     if t.get("source_hash") != kernel_source_hash() or t.get("workload") != workload:
         return None
     return t.get("traffic_bytes_per_launch")
 
 
+def host_cores():
+    """Host cores this process may use: its CPU affinity, capped by OMP_NUM_THREADS when that is set
+    (a one-GPU machine grants a share of the host's cores and sets it to that share)."""
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    omp = os.environ.get("OMP_NUM_THREADS")
+    if omp and omp.isdigit() and int(omp) > 0:
+        n = min(n, int(omp))
+    return max(1, n)
+
+
+# The forked oracle workers read the workload (and the post-append pool) that the
+# parent holds; fork shares those pages, so nothing is copied or pickled.
+_CPU_STATE = {}
+
+
+def _oracle_worker(job):
+    """One worker of the CPU baseline: the oracle on its own sequences, in order, until the budget.
+    The caller has limited BLAS to one thread (a forked worker inherits that setting; it must not
+    query the loaded libraries itself, which can block on a loader lock held at the fork)."""
+    import oracle
+    order, budget_s = job
+    wl, pool = _CPU_STATE["wl"], _CPU_STATE["pool"]
+    done = 0
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < budget_s:
+        oracle.attention_for_workload(wl, seqs=[int(order[done % len(order)])], pool=pool)
+        done += 1
+    return done, time.perf_counter() - t0
+
+
 def cpu_baseline(wl, budget_s, bytes_per_step):
-    """The oracle as it stands, single-threaded, on a bounded sample of sequences."""
+    """The oracle as it stands, timed on the host: on every core this process may use (one forked
+    worker per core, each on its own share of the sequences in a random order, BLAS at one thread)
+    and on one core, each for a bounded wall-clock sample. Must run before the process touches the
+    GPU, so that the workers are forks of a process without a device context."""
     if budget_s <= 0:
         return None
+    if any(k.startswith("ROCPROF") for k in os.environ) or "rocprof" in os.environ.get("LD_PRELOAD", ""):
+        # Under a profiler the preloaded library has already opened the device: no forks.
+        print("[bench] under a profiler: CPU baseline skipped", file=sys.stderr, flush=True)
+        return None
+    import multiprocessing as mp
     import numpy as np
     from threadpoolctl import threadpool_limits
-    import oracle
     from oracle.append import append_for_workload
 
-    pool = None
-    t_app = 0.0
+    pool, t_app = None, 0.0
     if wl.append:
         t0 = time.perf_counter()
         pool = append_for_workload(wl)
         t_app = time.perf_counter() - t0
-    # Sequences in a random order, in repeated passes, until the budget is spent.
+    _CPU_STATE.update(wl=wl, pool=pool)
     order = np.random.default_rng(0).permutation(wl.num_seqs)
-    done = 0
+    n = min(host_cores(), wl.num_seqs)
+    share = budget_s * 0.6
     with threadpool_limits(limits=1):
-        t0 = time.perf_counter()
-        while time.perf_counter() - t0 < budget_s:
-            oracle.attention_for_workload(wl, seqs=[int(order[done % wl.num_seqs])], pool=pool)
-            done += 1
-        el = time.perf_counter() - t0
-    seq_steps_per_s = done / (el + t_app * done / wl.num_seqs)
-    return {"value": round(bytes_per_step / wl.num_seqs * seq_steps_per_s / 1e9, 4), "unit": "GB/s",
-            "cores": 1, "kind": "oracle",
-            "sample": f"fp64 numpy oracle, {done} sequence-steps ({done / wl.num_seqs:.1f} passes over the "
-                      f"{wl.num_seqs} sequences of the workload in random order, {el:.1f} s, 1 thread"
-                      f"{', plus the append on the whole pool' if wl.append else ''}); scaled by the "
-                      f"step's algorithmic bytes per sequence",
-            "seq_steps_per_s": round(seq_steps_per_s, 3)}
+        with mp.get_context("fork").Pool(n) as workers:
+            res = workers.map(_oracle_worker, [(order[i::n], share) for i in range(n)])
+        done_one, el_one = _oracle_worker((order, budget_s - share))
+    done_all = sum(r[0] for r in res)
+    el_all = max(r[1] for r in res)
+    _CPU_STATE.clear()
+    # The append runs once per step over the whole pool; charge it per sequence-step.
+    rate = lambda done, el: done / (el + t_app * done / wl.num_seqs)
+    all_rate, one_rate = rate(done_all, el_all), rate(done_one, el_one)
+    per_seq = bytes_per_step / wl.num_seqs
+    app = ", plus the append on the whole pool" if wl.append else ""
+    return {"value": round(per_seq * all_rate / 1e9, 4), "unit": "GB/s", "cores": n, "kind": "oracle",
+            "sample": f"fp64 numpy oracle on {n} forked workers (one per host core, BLAS at one thread each), "
+                      f"{done_all} sequence-steps in {el_all:.1f} s over the {wl.num_seqs} sequences of the "
+                      f"workload in random order{app}; scaled by the step's algorithmic bytes per sequence",
+            "seq_steps_per_s": round(all_rate, 3),
+            "one_core": {"value": round(per_seq * one_rate / 1e9, 4), "unit": "GB/s", "cores": 1,
+                         "seq_steps_per_s": round(one_rate, 3),
+                         "sample": f"{done_one} sequence-steps in {el_one:.1f} s, one thread{app}"},
+            "host_cores_visible": os.cpu_count()}
 
 
 def _pmc_kib_per_dispatch(csv_path, kernel_substr, counter):
@@ -172,7 +228,7 @@ def _pmc_kib_per_dispatch(csv_path, kernel_substr, counter):
     return sum(vals) / len(vals), len(vals)
 
 
-def summarise_traffic(root):
+def summarise_traffic(root, workload):
     """FETCH_SIZE / WRITE_SIZE (KiB per dispatch) of the partial-attention kernel, scaled by the
     same counters' reading for a plain 1 GiB device copy (1 GiB read + 1 GiB written)."""
     f = lambda sub: os.path.join(root, sub, "pmc_counter_collection.csv")
@@ -183,7 +239,7 @@ def summarise_traffic(root):
     gib_kib = float(1 << 20)
     kf, kw = gib_kib / cfetch, gib_kib / cwrite       # true bytes per counted byte
     fetch_b, write_b = fetch * 1024 * kf, write * 1024 * kw
-    out = {"kernel": "attn_parts_kernel", "workload": "config2", "source_hash": kernel_source_hash(),
+    out = {"kernel": "attn_parts_kernel", "workload": workload, "source_hash": kernel_source_hash(),
            "fetch_kib_per_dispatch": round(fetch, 1), "write_kib_per_dispatch": round(write, 1),
            "dispatches": [n1, n2], "copy_fetch_kib_per_GiB": round(cfetch, 1),
            "copy_write_kib_per_GiB": round(cwrite, 1), "fetch_scale": round(kf, 4), "write_scale": round(kw, 4),
@@ -242,7 +298,7 @@ def prefill_bench(args):
     import paper_2606_26997_amd as rp
     from workloads import CONFIGS, make_prefill_workload
 
-    cfg = CONFIGS[args.config]
+    cfg = CONFIGS[args.config or 2]
     rng = np.random.default_rng(cfg.seed if args.seed is None else args.seed)
     if args.prefill_len is not None:
         P = np.full(cfg.groups, args.prefill_len)
@@ -277,18 +333,23 @@ def prefill_bench(args):
     torch.cuda.synchronize()
     ms = (time.perf_counter() - t0) / args.steps * 1e3
     attn_us = float(np.mean([a.elapsed_time(c) for a, c in ev])) * 1e3
-    # The timed launch's bytes: q, k, v read, out and lse written, and (bf16,
-    # one launch) the pages written.
-    attn_bytes = T * (Hq + 2 * Hkv + Hq) * d * 2 + T * Hq * 4 + (T * Hkv * d * 2 * eb if eb == 2 else 0)
+    # The timed call's bytes: q, k, v read, out and lse written, and the pages
+    # written (bf16: by the attention launch itself; fp8: by the page-write
+    # kernel that runs first, which reads k and v once more and writes the
+    # codes and the per-(page, kv-head) scales).
+    attn_bytes = T * (Hq + 2 * Hkv + Hq) * d * 2 + T * Hq * 4 + T * Hkv * d * 2 * eb
+    if eb == 1:
+        attn_bytes += T * Hkv * d * 2 * 2 + int(((P64 + 15) // 16).sum()) * Hkv * 8
     # Below the bf16 ridge (about 310 flop/B) the kernel is priced against HBM
     # bandwidth, above it against the dense bf16 MFMA peak.
     gbps_attn = attn_bytes / (attn_us * 1e-6) / 1e9
     tflops_attn = flops / (attn_us * 1e-6) / 1e12
+    kname = "prefill_attn_kernel" if eb == 2 else "prefill_kv_write_kernel + prefill_attn_kernel"
     if flops / attn_bytes < 310:
-        roof = {"kernel": "prefill_attn_kernel", "bound": "hbm", "achieved": round(gbps_attn, 1),
+        roof = {"kernel": kname, "bound": "hbm", "achieved": round(gbps_attn, 1),
                 "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(gbps_attn / HBM_PEAK_GBPS, 4)}
     else:
-        roof = {"kernel": "prefill_attn_kernel", "bound": "mfma", "achieved": round(tflops_attn, 1),
+        roof = {"kernel": kname, "bound": "mfma", "achieved": round(tflops_attn, 1),
                 "peak": 2500.0, "unit": "TFLOP/s", "frac": round(tflops_attn / 2500.0, 4)}
     roof.update({"traffic": None, "algorithmic_bytes_per_launch": int(attn_bytes), "flops_per_launch": flops,
                  "mfma_frac": round(tflops_attn / 2500.0, 4)})
@@ -296,7 +357,7 @@ def prefill_bench(args):
         "metric": "shared-prefix prefill: prompt tokens/s and achieved HBM GB/s (one prompt per group)",
         "value": round(T / (ms * 1e-3), 1), "unit": "prompt tokens/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "vs_baseline": None, "dtype": w.kv_dtype, "data": "synthetic",
         "config": {"workload": f"config{cfg.cid} prompts" + (f" of {args.prefill_len} tokens" if args.prefill_len else ""),
                    "groups": int(cfg.groups), "prompt_tokens": T, "q_heads": Hq, "kv_heads": Hkv, "head_dim": d,
                    "kv_dtype": w.kv_dtype},
@@ -684,7 +745,7 @@ def main():
         read_ceiling(args.steps)
         return
     if args.traffic_from:
-        summarise_traffic(args.traffic_from)
+        summarise_traffic(args.traffic_from, f"config{args.config or 2}")
         return
     if args.prefill:
         prefill_bench(args)
@@ -699,15 +760,44 @@ def main():
         grpo_bench(args)
         return
 
-    import paper_2606_26997_amd as rp
     from workloads import CONFIGS, make_config_workload
 
-    cfg = CONFIGS[args.config]
-    t0 = time.perf_counter()
-    wl = make_config_workload(cfg, seed=args.seed)
-    gen_s = time.perf_counter() - t0
-    print(f"[bench] config{cfg.cid} generated in {gen_s:.1f}s: {wl.num_seqs} seqs, "
-          f"{wl.num_pages} pages", file=sys.stderr, flush=True)
+    # Phase 1, host only: every workload and its oracle CPU baseline, before anything touches the
+    # GPU (the baseline forks its workers). The headline workload is config 2, the Qwen3-1.7B
+    # layer shape; the default run also reports configs 3-5 (one line each on stderr, first).
+    cids = [args.config] if args.config is not None else [3, 4, 5, 2]
+    prepared = []
+    for cid in cids:
+        cfg = CONFIGS[cid]
+        t0 = time.perf_counter()
+        wl = make_config_workload(cfg, seed=args.seed)
+        print(f"[bench] config{cid} generated in {time.perf_counter() - t0:.1f}s: {wl.num_seqs} seqs, "
+              f"{wl.num_pages} pages", file=sys.stderr, flush=True)
+        cpu = None
+        if args.cpu_seconds > 0:
+            budget = args.cpu_seconds if cid == cids[-1] else args.cpu_seconds / 2
+            t0 = time.perf_counter()
+            cpu = cpu_baseline(wl, budget, byte_model(wl)["total"])
+            if cpu is not None:
+                print(f"[bench] config{cid} oracle CPU baseline: {cpu['value']} GB/s on {cpu['cores']} cores "
+                      f"({time.perf_counter() - t0:.1f}s)", file=sys.stderr, flush=True)
+        prepared.append((cfg, wl, cpu))
+
+    # Phase 2: the GPU, one workload at a time.
+    for i, (cfg, wl, cpu) in enumerate(prepared):
+        line = decode_bench(cfg, wl, cpu, args)
+        prepared[i] = None
+        del wl
+        last = i == len(prepared) - 1
+        print(json.dumps(line), file=sys.stdout if last else sys.stderr, flush=True)
+
+
+def decode_bench(cfg, wl, cpu, args):
+    """One workload's decode-attention step on the GPU: timed steps, per-kernel breakdown, roofline."""
+    import numpy as np
+    import torch
+    import paper_2606_26997_amd as rp
+
     torch.cuda.set_device(0)
     batch = rp.DeviceBatch.from_workload(wl, device="cuda:0")
     bm = byte_model(wl)
@@ -758,16 +848,13 @@ def main():
     samples["parts_timed"] = parts_samples
     spread = {name: {"median": round(float(np.median(v)), 2), "p10": round(float(np.percentile(v, 10)), 2),
                      "p90": round(float(np.percentile(v, 90)), 2)} for name, v in samples.items()}
+    del batch
+    torch.cuda.empty_cache()
 
     gbps = bm["total"] / (ms_per_step * 1e-3) / 1e9
     achieved = bm["parts_kernel"] / (parts_us * 1e-6) / 1e9
     traffic = load_traffic(f"config{cfg.cid}") if args.seed is None else None
-    cpu = None
-    if args.cpu_seconds > 0:
-        print("[bench] timing the oracle CPU baseline", file=sys.stderr, flush=True)
-        cpu = cpu_baseline(wl, args.cpu_seconds, bm["total"])
-
-    line = {
+    return {
         "metric": METRIC,
         "value": round(gbps, 2),
         "unit": "GB/s",
@@ -798,7 +885,6 @@ def main():
                      "traffic": traffic, "algorithmic_bytes_per_launch": int(bm["parts_kernel"])},
         "cpu_baseline": cpu,
     }
-    print(json.dumps(line), flush=True)
 
 
 if __name__ == "__main__":

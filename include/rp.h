@@ -116,7 +116,12 @@ const char* rp_last_error(void);
  * a later row keeps the scale if amax <= 448 * scale, otherwise sets
  * scale = amax / 448 and requantises rows 0..r-1 from code * old_scale; the
  * row is stored as e4m3(x / scale), round to nearest even, saturated at 448.
- * Two sequences must not append into the same (page, kv-head). */
+ * A NaN element of x does not enter amax and is stored as the saturated code
+ * with its sign (0x7E or 0xFE); the NaN code is never written.
+ * Two sequences must not append into the same (page, kv-head).
+ * Defined by the decode step of the rollout's decode workers (paper,
+ * Section 4): every generated token's K and V join its sequence's cache
+ * before attention reads them. */
 rp_status rp_kv_append(const rp_paged_kv* kv, const rp_group_layout* layout,
                        const void* k_new, const void* v_new, hipStream_t stream);
 
@@ -157,7 +162,10 @@ rp_status rp_group_decode_attn_workspace_size(const rp_paged_kv* kv,
                                               const rp_group_layout* layout,
                                               size_t* bytes);
 
-/* Group decode attention (the definition at the top of this file).
+/* Group decode attention (the definition at the top of this file): one
+ * decode step of every sequence of the rollout batch (paper, Section 4, the
+ * rollout node's decode workers), the K responses of a GRPO group sharing
+ * their prompt's KV (Section 2.1; Section 5.1 samples K = 8).
  * q:   bf16 [num_seqs][num_q_heads][head_dim], 16-byte aligned.
  * out: bf16 [num_seqs][num_q_heads][head_dim], 16-byte aligned.
  * lse: fp32 [num_seqs][num_q_heads], natural log; may be NULL.
@@ -170,7 +178,11 @@ rp_status rp_group_decode_attn(const rp_paged_kv* kv, const rp_group_layout* lay
                                const void* q, float softmax_scale, void* out, float* lse,
                                void* workspace, size_t workspace_bytes, hipStream_t stream);
 
-/* Log-sum-exp merge of partial attention results over disjoint key subsets.
+/* Log-sum-exp merge of partial attention results over disjoint key subsets
+ * (the step that makes splitting a sequence's keys exact: attention over a
+ * union of disjoint key sets is the lse-weighted mean of the parts; it is
+ * how the group-prefix parts of Section 2.1's shared prompt join each
+ * response's own parts).
  * o_parts: fp32 [total_parts][head_dim] (16-byte aligned), lse_parts: fp32 [total_parts] (natural
  * log, -inf marks an empty part whose o is ignored); row r owns parts
  * row_part_offsets[r] .. row_part_offsets[r+1]-1 (int32 CSR, [num_rows + 1]).
@@ -204,9 +216,10 @@ typedef struct {
 /* Write every group's prompt K/V into its prefix pages. bf16 pools copy the
  * rows. fp8 pools give each (page, kv-head) of a prompt, in fp32,
  * scale = amax / 448 over the page's written rows (1.0 when amax = 0) and
- * store e4m3(x / scale) (round to nearest even, saturating at 448); rows past
- * a prompt's end are not written. k, v: bf16 [T][Hkv][head_dim], 16-byte
- * aligned. Prompts must not share pages. */
+ * store e4m3(x / scale) (round to nearest even, saturating at 448; a NaN
+ * element does not enter amax and is stored as the saturated code with its
+ * sign); rows past a prompt's end are not written. k, v: bf16
+ * [T][Hkv][head_dim], 16-byte aligned. Prompts must not share pages. */
 rp_status rp_prefill_kv_write(const rp_paged_kv* kv, const rp_prefill_layout* layout,
                               const void* k, const void* v, hipStream_t stream);
 

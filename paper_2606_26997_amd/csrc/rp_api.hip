@@ -43,16 +43,17 @@ rp_status check_kv(const rp_paged_kv* kv) {
   if (kv->page_size != rp::kPage) return fail(RP_ERR_UNSUPPORTED, "page_size %d unsupported (16 only)", kv->page_size);
   if (kv->head_dim != 64 && kv->head_dim != 128)
     return fail(RP_ERR_UNSUPPORTED, "head_dim %d unsupported (64 or 128)", kv->head_dim);
-  if (kv->kv_dtype == RP_KV_BF16) {
+  const int dtype = rp::enum_bits(kv->kv_dtype);
+  if (dtype == RP_KV_BF16) {
     if (kv->k_scale != nullptr || kv->v_scale != nullptr)
       return fail(RP_ERR_INVALID_ARG, "k_scale/v_scale must be NULL for bf16 KV");
-  } else if (kv->kv_dtype == RP_KV_FP8_E4M3) {
+  } else if (dtype == RP_KV_FP8_E4M3) {
     if (kv->k_scale == nullptr || kv->v_scale == nullptr)
       return fail(RP_ERR_INVALID_ARG, "k_scale/v_scale required for fp8 KV");
     if (!aligned(kv->k_scale, 4) || !aligned(kv->v_scale, 4))
       return fail(RP_ERR_INVALID_ARG, "k_scale/v_scale must be 4-byte aligned");
   } else {
-    return fail(RP_ERR_UNSUPPORTED, "kv_dtype %d unsupported", (int)kv->kv_dtype);
+    return fail(RP_ERR_UNSUPPORTED, "kv_dtype %d unsupported", dtype);
   }
   return RP_OK;
 }
@@ -96,7 +97,7 @@ rp_status check_shape(const rp_paged_kv* kv, const rp_group_layout* l, Shape* sh
   sh->max_pp = l->max_prefix_pages;
   sh->max_rp = l->max_resp_pages;
   sh->num_pages = kv->num_pages;
-  sh->fp8 = kv->kv_dtype == RP_KV_FP8_E4M3;
+  sh->fp8 = rp::enum_bits(kv->kv_dtype) == RP_KV_FP8_E4M3;
   return RP_OK;
 }
 
@@ -214,7 +215,7 @@ rp::AttnArgs attn_args(const rp_paged_kv* kv, const rp_group_layout* l, const vo
 extern "C" {
 
 const char* rp_status_string(rp_status status) {
-  switch (status) {
+  switch (rp::enum_bits(status)) {
     case RP_OK: return "RP_OK: success";
     case RP_ERR_INVALID_ARG: return "RP_ERR_INVALID_ARG: invalid argument";
     case RP_ERR_UNSUPPORTED: return "RP_ERR_UNSUPPORTED: unsupported configuration";
@@ -496,7 +497,7 @@ rp_status rp_prefill_kv_write(const rp_paged_kv* kv, const rp_prefill_layout* l,
     return fail(RP_ERR_INVALID_ARG, "k/v must be non-NULL and 16-byte aligned");
   a.k = k;
   a.v = v;
-  hipError_t e = rp::launch_prefill_kv_write(a, kv->head_dim, kv->kv_dtype == RP_KV_FP8_E4M3, stream);
+  hipError_t e = rp::launch_prefill_kv_write(a, kv->head_dim, rp::enum_bits(kv->kv_dtype) == RP_KV_FP8_E4M3, stream);
   return e == hipSuccess ? RP_OK : hip_fail(e, "prefill KV write kernel launch");
 }
 
@@ -524,7 +525,7 @@ static rp_status prefill_impl(const rp_paged_kv* kv, const rp_prefill_layout* l,
   a.qk_scale = softmax_scale * rp::kLog2e;
   a.out = out;
   a.lse = lse;
-  const bool fp8 = kv->kv_dtype == RP_KV_FP8_E4M3;
+  const bool fp8 = rp::enum_bits(kv->kv_dtype) == RP_KV_FP8_E4M3;
   if (pages && fp8) {
     hipError_t e = rp::launch_prefill_kv_write(a, kv->head_dim, true, stream);
     if (e != hipSuccess) return hip_fail(e, "prefill KV write kernel launch");

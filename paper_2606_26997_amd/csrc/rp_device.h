@@ -113,19 +113,21 @@ __device__ inline float e4m3_to_f32(uint32_t code) {
   return __builtin_amdgcn_cvt_f32_fp8((int)code, 0);
 }
 
-// fp32 -> e4m3fn code, round to nearest even, saturating at +-448.
+// fp32 -> e4m3fn code, round to nearest even, saturating at +-448. A NaN
+// input (inf included among |x| >= 448) also takes the saturated code, with
+// its sign bit: the append and page-write rules never store the NaN code.
 __device__ inline uint32_t f32_to_e4m3(float x) {
   const uint32_t u = __float_as_uint(x);
   const uint32_t sign = (u >> 24) & 0x80u;
   const uint32_t a = u & 0x7FFFFFFFu;
   uint32_t code;
-  if (a >= 0x43E00000u) {                 // |x| >= 448 (or inf)
+  if (a >= 0x43E00000u) {                 // |x| >= 448, inf or NaN
     code = 0x7Eu;
   } else if (a < 0x3C800000u) {           // |x| < 2^-6: subnormal grid of step 2^-9
     float q = __builtin_rintf(__uint_as_float(a) * 512.0f);  // exact scaling, RNE
     code = (uint32_t)q;                   // 0..8; 8 encodes 2^-6 exactly
   } else {
-    const uint32_t e = (a >> 23) - 127u + 7u;   // 1..8
+    const uint32_t e = (a >> 23) - 127u + 7u;   // 1..15 (2^-6 <= |x| < 448)
     const uint32_t m = a & 0x7FFFFFu;
     const uint32_t keep = m >> 20, rem = m & 0xFFFFFu;
     const uint32_t up = (rem > 0x80000u) || (rem == 0x80000u && (keep & 1u));

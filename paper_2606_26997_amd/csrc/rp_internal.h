@@ -5,6 +5,7 @@
 #include <stdint.h>
 
 #include "rp_device.h"
+#include "rp_host.h"
 
 namespace rp {
 

@@ -51,8 +51,9 @@ extern "C" rp_status rp_sched_simulate(const rp_sched_config* cfg, const int32_t
   if (cfg == nullptr || prompt_lens == nullptr || resp_lens == nullptr || summary == nullptr)
     return rp::set_error(RP_ERR_INVALID_ARG, "config, prompt_lens, resp_lens and summary must be non-NULL");
   const int R = cfg->num_groups, K = cfg->group_size, U = cfg->update_groups;
-  const bool fgd = cfg->mode == RP_SCHED_CGP_FGD, slime = cfg->mode == RP_SCHED_SLIME;
-  if (cfg->mode != RP_SCHED_SLIME && cfg->mode != RP_SCHED_CGP && !fgd)
+  const int mode = rp::enum_bits(cfg->mode);
+  const bool fgd = mode == RP_SCHED_CGP_FGD, slime = mode == RP_SCHED_SLIME;
+  if (mode != RP_SCHED_SLIME && mode != RP_SCHED_CGP && !fgd)
     return rp::set_error(RP_ERR_INVALID_ARG, "unknown scheduling mode");
   if (R < 1 || K < 1 || U < 1 || R % U != 0 || cfg->max_running < 1 || (int64_t)R * K > INT32_MAX)
     return rp::set_error(RP_ERR_INVALID_ARG,

@@ -1,4 +1,9 @@
 """Shared helpers for GPU parity tests: run the HIP path, run the oracle, compare."""
+import os
+import sys
+import time
+from concurrent.futures import ThreadPoolExecutor
+
 import numpy as np
 import torch
 
@@ -35,6 +40,40 @@ def run_hip(wl, batch=None):
 def run_oracle(wl, seqs=None):
     pool = append_for_workload(wl) if wl.append else None
     out, lse = oracle.attention_for_workload(wl, seqs=seqs, pool=pool)
+    return out, lse, pool
+
+
+def oracle_threads():
+    """Oracle worker threads: the host's CPU share (16 on a one-GPU machine), at most 16."""
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    return max(1, min(16, n, int(os.environ.get("OMP_NUM_THREADS", n))))
+
+
+def run_oracle_all(wl, pool=None, chunk=16, label=""):
+    """Oracle result for every sequence of ``wl``, computed in chunks of sequences by a thread pool
+    over the one host copy of the pool (numpy's gathers and BLAS calls release the GIL for part of
+    the work). Prints a progress line per quarter so that a long comparison is visibly alive."""
+    from threadpoolctl import threadpool_limits
+    if wl.append and pool is None:
+        pool = append_for_workload(wl)
+    S = wl.num_seqs
+    chunks = [list(range(i, min(S, i + chunk))) for i in range(0, S, chunk)]
+    out = np.zeros((S, wl.num_q_heads, wl.head_dim))
+    lse = np.full((S, wl.num_q_heads), -np.inf)
+    t0 = time.perf_counter()
+    done = 0
+    with threadpool_limits(limits=1), ThreadPoolExecutor(oracle_threads()) as ex:
+        futs = [(c, ex.submit(oracle.attention_for_workload, wl, seqs=c, pool=pool)) for c in chunks]
+        for i, (c, f) in enumerate(futs):
+            o, l = f.result()
+            out[c[0]:c[-1] + 1], lse[c[0]:c[-1] + 1] = o, l
+            done += len(c)
+            if (i + 1) % max(1, len(futs) // 4) == 0 or i + 1 == len(futs):
+                print(f"[oracle] {label} {done}/{S} sequences, {time.perf_counter() - t0:.1f} s", flush=True)
+                sys.stdout.flush()
     return out, lse, pool
 
 

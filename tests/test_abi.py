@@ -250,3 +250,30 @@ def test_grpo_advantage_argument_checks():
     assert call(eps=-1e-6) == rp.RP_ERR_INVALID_ARG and "eps_std" in rp.last_error()
     assert call(eps=float("inf")) == rp.RP_ERR_INVALID_ARG
     assert call(R=0, r=None, adv=None) == rp.RP_OK
+
+
+def _no_gpu():
+    import torch
+    return not torch.cuda.is_available()
+
+
+@pytest.mark.skipif(not _no_gpu(), reason="forces a HIP runtime failure; only meaningful without a GPU")
+def test_hip_failure_maps_to_rp_err_hip():
+    """Well-formed calls on a host without a GPU: the first HIP runtime call fails, and the library
+    reports RP_ERR_HIP with the runtime's text instead of crashing. rp_plan fails in its device
+    query, rp_kv_append and rp_lse_combine in their kernel launches."""
+    lib = rp.load()
+    kv, lay = _kv(), _layout()
+    st, n = _ws_size(kv, lay)
+    assert st == rp.RP_OK and n > 0
+    st = lib.rp_plan(ctypes.byref(kv), ctypes.byref(lay), A, n, None)
+    assert st == rp.RP_ERR_HIP, rp.status_string(st)
+    assert "hipGetDevice" in rp.last_error()
+    st = lib.rp_kv_append(ctypes.byref(kv), ctypes.byref(lay), A, A, None)
+    assert st == rp.RP_ERR_HIP and "append kernel launch" in rp.last_error(), rp.last_error()
+    st = lib.rp_lse_combine(A, A, A, 4, 64, A, None, None)
+    assert st == rp.RP_ERR_HIP and "combine kernel launch" in rp.last_error(), rp.last_error()
+    # The binding turns the code into an exception carrying the same detail.
+    with pytest.raises(rp.RpError) as e:
+        B._check(lib.rp_plan(ctypes.byref(kv), ctypes.byref(lay), A, n, None), "rp_plan")
+    assert e.value.status == rp.RP_ERR_HIP and "hipGetDevice" in str(e.value)

@@ -95,13 +95,21 @@ def test_prefill_pages_and_attention(case):
     _check_attn(b, w, name)
 
 
-def test_qwen_layer_prompts_full():
-    # The decode benchmark's prompts: 32 groups, prefix U[64, 512], Hq=16, Hkv=8, d=128, K x 0.5.
-    _say("prefill 32 groups x U[64,512]")
+@pytest.mark.parametrize("one_call", [False, True], ids=["two-calls", "rp_prefill"])
+def test_qwen_layer_prompts_full(one_call):
+    # The decode benchmark's prompts: 32 groups, prefix U[64, 512], Hq=16, Hkv=8, d=128, K x 0.5,
+    # through the two calls and through rp_prefill (the launch the prefill bench times).
+    import paper_2606_26997_amd as rp
+    _say(f"prefill 32 groups x U[64,512], {'rp_prefill' if one_call else 'two calls'}")
     rng = np.random.default_rng(1002)
     w = make_prefill_workload(num_q_heads=16, num_kv_heads=8, head_dim=128,
                               prefix_lens=rng.integers(64, 513, 32), seed=1002, k_mult=0.5)
-    b = _run(w)
+    if one_call:
+        b = rp.PrefillBatch.from_workload(w)
+        b.prefill()
+        torch.cuda.synchronize()
+    else:
+        b = _run(w)
     _check_pages(b, w, "qwen-prompts")
     _check_attn(b, w, "qwen-prompts")
 

@@ -4,8 +4,10 @@ q (and the optional k copy) is compared with the fp64 oracle's correctly
 rounded bf16 bits: every element within one bf16 ulp, and all but a tiny
 fraction bit-identical (the kernel also computes in fp64 and rounds once).
 The pool after the append is compared byte for byte (codes and scales) with
-the append oracle applied to the kernel's own rotated k, so a rare one-ulp k
-difference cannot hide a wrong slot, page or scale decision. End-to-end
+the pure oracle: the append of the oracle's own rotated k and of v. Only the
+slots of a (sequence, kv-head) whose kernel k differs from the oracle's k by
+its one allowed ulp are named exceptions; they are listed, and there the pool
+must hold the append of the kernel's k instead. End-to-end
 cases run the whole decode step (prep, then attention over the advanced
 lengths) at the frontier operating point of 2 groups x 8 samples and compare
 it with the oracle's attention at the usual tolerances.
@@ -74,11 +76,39 @@ def _oracle_prep(wl, x, resp_lens=None):
 
 
 def _oracle_pool(wl, x, k_bits, seqs=None):
-    """Append oracle on the kernel's rotated k (only for sequences ``seqs``, default all)."""
+    """Append oracle of ``k_bits`` and v (only for sequences ``seqs``, default all)."""
     idx = np.arange(wl.num_seqs) if seqs is None else np.asarray(seqs)
     return oracle.kv_append(k_pages=wl.k_pages, v_pages=wl.v_pages, k_scale=wl.k_scale, v_scale=wl.v_scale,
                             kv_dtype=wl.kv_dtype, page_size=16, resp_lens=wl.resp_lens[idx],
                             resp_block_table=wl.resp_block_table[idx], k_new=k_bits[idx], v_new=x.v_in[idx])
+
+
+def _check_pool(b, wl, x, k_gpu, k_ref, label, seqs=None):
+    """The pool after the kernel's append against the pure oracle (its own k). A (sequence, kv-head)
+    whose kernel k is one ulp off the oracle's in some element (allowed by the k check) is a named
+    exception: there the k slot (bf16: the row; fp8: the whole (page, kv-head) block and its scale,
+    which that row's amax may move) must equal the append of the kernel's k."""
+    dt = wl.kv_dtype
+    idx = np.arange(wl.num_seqs) if seqs is None else np.asarray(seqs)
+    ref = [np.array(a, copy=True) for a in _oracle_pool(wl, x, k_ref, seqs) if a is not None]
+    off = np.argwhere((k_gpu[idx] != k_ref[idx]).any(axis=2))      # rows of idx, kv-head
+    if off.size:
+        print(f"[case] {label}: k differs by one ulp at (sequence, kv-head) {[(int(idx[i]), int(h)) for i, h in off]}",
+              flush=True)
+        alt = [a for a in _oracle_pool(wl, x, k_gpu, seqs) if a is not None]
+        for i, h in off:
+            s = int(idx[i])
+            t = int(wl.resp_lens[s])
+            page = int(wl.resp_block_table[s][t // 16])
+            if dt == "bf16":
+                ref[0][page, h, t % 16] = alt[0][page, h, t % 16]
+            else:
+                ref[0][page, h] = alt[0][page, h]
+                ref[2][page, h] = alt[2][page, h]
+    got = _pool_bytes(b, dt)
+    for g, r, what in zip(got, ref, ("k pages", "v pages", "k scales", "v scales")):
+        np.testing.assert_array_equal(g, r, err_msg=f"{label}: {what}")
+    return got
 
 
 CASES = [
@@ -104,10 +134,7 @@ def test_qk_prep_and_append(case):
     _check_bits(_bits(b.q), qb, f"{name} q")
     k_gpu = _bits(b.k_out)
     _check_bits(k_gpu, kb, f"{name} k")
-    ref = _oracle_pool(wl, x, k_gpu)
-    got = _pool_bytes(b, dt)
-    for g, r, what in zip(got, ref, ("k pages", "v pages", "k scales", "v scales")):
-        np.testing.assert_array_equal(g, r, err_msg=f"{name}: {what}")
+    got = _check_pool(b, wl, x, k_gpu, kb, name)
     if dt == "fp8":
         # The case exercises the scale branch it is named for on rows r > 0.
         raised = []
@@ -122,7 +149,7 @@ def test_qk_prep_and_append(case):
     b.qk_prep()
     torch.cuda.synchronize()
     assert np.array_equal(_bits(b.q), q1)
-    for g, r in zip(_pool_bytes(b, dt), ref):
+    for g, r in zip(_pool_bytes(b, dt), got):
         assert np.array_equal(g, r), name
 
 
@@ -157,9 +184,7 @@ def test_qk_prep_slot_outside_table_gets_q_but_no_append():
     qb, kb = _oracle_prep(wl, x, resp_lens=rl)
     _check_bits(_bits(b.q), qb, "q")
     _check_bits(_bits(b.k_out), kb, "k")
-    ref = _oracle_pool(wl, x, _bits(b.k_out), seqs=[0, 2])
-    for g, r in zip(_pool_bytes(b, "bf16"), ref):
-        np.testing.assert_array_equal(g, r)
+    _check_pool(b, wl, x, _bits(b.k_out), kb, "slot outside the table", seqs=[0, 2])
 
 
 @pytest.mark.parametrize("kv_dtype", ["bf16", "fp8"])
@@ -177,8 +202,7 @@ def test_qk_prep_large_batch_one_block_per_sequence(kv_dtype):
     _check_bits(_bits(b.q), qb, "q")
     k_gpu = _bits(b.k_out)
     _check_bits(k_gpu, kb, "k")
-    for g, r in zip(_pool_bytes(b, kv_dtype), _oracle_pool(wl, x, k_gpu)):
-        np.testing.assert_array_equal(g, r)
+    _check_pool(b, wl, x, k_gpu, kb, f"1100 sequences {kv_dtype}")
 
 
 @pytest.mark.parametrize("kv_dtype", ["bf16", "fp8"])
