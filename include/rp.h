@@ -178,6 +178,29 @@ rp_status rp_group_decode_attn(const rp_paged_kv* kv, const rp_group_layout* lay
                                const void* q, float softmax_scale, void* out, float* lse,
                                void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* Bytes of device scratch behind rp_group_decode_attn_noalloc (64 MiB): a
+ * static array in the library, one copy per GPU, held until the process
+ * ends. */
+#define RP_NOALLOC_SCRATCH_BYTES (64u << 20)
+
+/* rp_group_decode_attn without a workspace, for callers that cannot allocate
+ * device memory: code under HIP graph capture, tight serving loops and
+ * harnesses that forbid hipMalloc. The plan and the partial results live in
+ * the library's static scratch of RP_NOALLOC_SCRATCH_BYTES on the current
+ * device (the same kernels and results as rp_group_decode_attn, bit for bit).
+ * Nothing is allocated; the first call on a device looks up that device's
+ * scratch address once. Layouts whose workspace
+ * (rp_group_decode_attn_workspace_size) exceeds the scratch are refused with
+ * RP_ERR_WORKSPACE before anything is launched: 256 sequences with 4096-token
+ * responses fit (21 MB), 1024 sequences of 8192 do not.
+ * All calls on one GPU share its scratch: calls that overlap in time on one
+ * GPU (different streams, host threads or processes sharing a context) race
+ * and give wrong results; serialise them. Arguments and errors otherwise as
+ * rp_group_decode_attn. */
+rp_status rp_group_decode_attn_noalloc(const rp_paged_kv* kv, const rp_group_layout* layout,
+                                       const void* q, float softmax_scale, void* out, float* lse,
+                                       hipStream_t stream);
+
 /* Log-sum-exp merge of partial attention results over disjoint key subsets
  * (the step that makes splitting a sequence's keys exact: attention over a
  * union of disjoint key sets is the lse-weighted mean of the parts; it is

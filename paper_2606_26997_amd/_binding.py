@@ -24,12 +24,13 @@ RP_ERR_HIP = 4
 RP_ERR_LAYOUT = 5
 RP_KV_BF16 = 0
 RP_KV_FP8_E4M3 = 1
+RP_NOALLOC_SCRATCH_BYTES = 64 << 20   # include/rp.h: static scratch of rp_group_decode_attn_noalloc
 
 EXPORTED = ("rp_status_string", "rp_last_error", "rp_kv_append",
             "rp_group_decode_attn_workspace_size", "rp_group_decode_attn", "rp_lse_combine",
             "rp_plan", "rp_attn_parts", "rp_combine_parts", "rp_plan_layout", "rp_validate_layout",
             "rp_prefill_kv_write", "rp_prefill_attn", "rp_decode_qk_prep", "rp_sched_simulate",
-            "rp_grpo_advantage", "rp_prefill")
+            "rp_grpo_advantage", "rp_prefill", "rp_group_decode_attn_noalloc")
 RP_SCHED_MODES = {"slime": 0, "cgp": 1, "cgp_fgd": 2}
 
 
@@ -101,6 +102,7 @@ def load() -> ctypes.CDLL:
         "rp_kv_append": (ctypes.c_int, [P, P, P, P, P]),
         "rp_group_decode_attn_workspace_size": (ctypes.c_int, [P, P, ctypes.POINTER(ctypes.c_size_t)]),
         "rp_group_decode_attn": (ctypes.c_int, [P, P, P, F32, P, P, P, ctypes.c_size_t, P]),
+        "rp_group_decode_attn_noalloc": (ctypes.c_int, [P, P, P, F32, P, P, P]),
         "rp_lse_combine": (ctypes.c_int, [P, P, P, I32, I32, P, P, P]),
         "rp_plan": (ctypes.c_int, [P, P, P, ctypes.c_size_t, P]),
         "rp_attn_parts": (ctypes.c_int, [P, P, P, F32, P, ctypes.c_size_t, P]),
@@ -214,6 +216,13 @@ def group_decode_attn(kv, layout, q, softmax_scale, out, lse, workspace, stream=
                                        float(softmax_scale), _ptr(out), _ptr(lse), _ptr(workspace),
                                        _ws_bytes(workspace), _stream(stream)),
            "rp_group_decode_attn")
+
+
+def group_decode_attn_noalloc(kv, layout, q, softmax_scale, out, lse, stream=None) -> None:
+    """rp_group_decode_attn on the library's static scratch (no workspace, nothing allocated)."""
+    _check(load().rp_group_decode_attn_noalloc(ctypes.byref(kv), ctypes.byref(layout), _ptr(q),
+                                               float(softmax_scale), _ptr(out), _ptr(lse), _stream(stream)),
+           "rp_group_decode_attn_noalloc")
 
 
 def plan(kv, layout, workspace, stream=None) -> None:

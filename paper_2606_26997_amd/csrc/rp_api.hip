@@ -6,6 +6,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 
 #include "rp.h"
 #include "rp_internal.h"
@@ -149,6 +150,34 @@ rp_status device_cus(int* cus) {
     cache[dev].store(n, std::memory_order_relaxed);
   }
   *cus = n;
+  return RP_OK;
+}
+
+// Scratch of rp_group_decode_attn_noalloc: the work plan and partial results
+// live in this device array instead of a caller workspace. Each GPU holds its
+// own copy for the life of the process; its name is only a host-side handle,
+// so host code uses the device address looked up once per device below.
+__device__ __align__(256) static unsigned char scratch[RP_NOALLOC_SCRATCH_BYTES];
+
+rp_status scratch_address(void** out) {
+  static std::atomic<void*> addr[64];
+  static std::mutex lookup;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= 64) return fail(RP_ERR_UNSUPPORTED, "device %d out of range", dev);
+  void* p = addr[dev].load(std::memory_order_acquire);
+  if (p == nullptr) {
+    std::lock_guard<std::mutex> lock(lookup);
+    p = addr[dev].load(std::memory_order_relaxed);
+    if (p == nullptr) {
+      e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));  // with device `dev` current
+      if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+      if (p == nullptr || !aligned(p, 256)) return fail(RP_ERR_HIP, "scratch has no usable device address");
+      addr[dev].store(p, std::memory_order_release);
+    }
+  }
+  *out = p;
   return RP_OK;
 }
 
@@ -320,6 +349,28 @@ rp_status rp_group_decode_attn(const rp_paged_kv* kv, const rp_group_layout* l, 
   st = rp_attn_parts(kv, l, q, softmax_scale, ws, ws_bytes, stream);
   if (st != RP_OK) return st;
   return rp_combine_parts(kv, l, out, lse, ws, ws_bytes, stream);
+}
+
+rp_status rp_group_decode_attn_noalloc(const rp_paged_kv* kv, const rp_group_layout* l, const void* q,
+                                       float softmax_scale, void* out, float* lse, hipStream_t stream) {
+  g_err[0] = 0;
+  Shape sh;
+  rp_status st = check_shape(kv, l, &sh);
+  if (st != RP_OK) return st;
+  WsLayout w;
+  if (!ws_layout(sh, &w)) return fail(RP_ERR_UNSUPPORTED, "layout too large for the work plan");
+  if (sh.S == 0) return RP_OK;
+  if (w.total > (size_t)RP_NOALLOC_SCRATCH_BYTES)
+    return fail(RP_ERR_WORKSPACE,
+                "this layout needs %zu bytes of scratch; the library's static scratch holds %zu "
+                "(use rp_group_decode_attn with a workspace)",
+                w.total, (size_t)RP_NOALLOC_SCRATCH_BYTES);
+  void* ws = nullptr;
+  st = scratch_address(&ws);
+  if (st != RP_OK) return st;
+  // The same three launches as rp_group_decode_attn. The plan overwrites every
+  // entry the attention and combine kernels read, so nothing needs clearing.
+  return rp_group_decode_attn(kv, l, q, softmax_scale, out, lse, ws, RP_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 rp_status rp_lse_combine(const float* o_parts, const float* lse_parts, const int32_t* row_part_offsets,

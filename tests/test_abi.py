@@ -277,3 +277,23 @@ def test_hip_failure_maps_to_rp_err_hip():
     with pytest.raises(rp.RpError) as e:
         B._check(lib.rp_plan(ctypes.byref(kv), ctypes.byref(lay), A, n, None), "rp_plan")
     assert e.value.status == rp.RP_ERR_HIP and "hipGetDevice" in str(e.value)
+
+
+def test_noalloc_scratch_limit_and_refusal():
+    """The binding's scratch size is the header's, and a layout whose workspace exceeds it is refused
+    before anything reaches the HIP runtime."""
+    text = open(HEADER).read()
+    m = re.search(r"#define RP_NOALLOC_SCRATCH_BYTES \((\d+)u << (\d+)\)", text)
+    assert m and int(m.group(1)) << int(m.group(2)) == rp.RP_NOALLOC_SCRATCH_BYTES
+    kv = _kv(num_kv_heads=8, head_dim=128)
+    lay = _layout(num_seqs=1024, num_groups=64, num_q_heads=16, mpp=16, mrp=513)
+    st, need = _ws_size(kv, lay)
+    assert st == rp.RP_OK and need > rp.RP_NOALLOC_SCRATCH_BYTES
+    lib = rp.load()
+    st = lib.rp_group_decode_attn_noalloc(ctypes.byref(kv), ctypes.byref(lay), A, ctypes.c_float(0.1), A, None,
+                                          None)
+    assert st == rp.RP_ERR_WORKSPACE and "static scratch" in rp.last_error()
+    assert lib.rp_group_decode_attn_noalloc(ctypes.byref(kv), ctypes.byref(_layout(num_seqs=0, num_q_heads=16)), None,
+                                            ctypes.c_float(0.1), None, None, None) == rp.RP_OK
+    assert lib.rp_group_decode_attn_noalloc(ctypes.byref(_kv(head_dim=96)), ctypes.byref(lay), A,
+                                            ctypes.c_float(0.1), A, None, None) == rp.RP_ERR_UNSUPPORTED
