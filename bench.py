@@ -383,10 +383,14 @@ def _model_step_ms(b, steps, layers=None, min_bytes=2e9):
     kvs = [rp.paged_kv(kp, vp) for kp, vp in pools]
 
     def model_step():
-        rp.plan(kvs[0], b.attn_layout, b.workspace)
+        # The first layer's prep also plans the step (one launch for small batches).
         for l in range(layers):
             kv = kvs[l % copies]
-            rp.decode_qk_prep(kv, b.append_layout, b.q_in, b.k_in, b.v_in, b.q_norm_w, b.k_norm_w, b.q, None)
+            if l == 0:
+                rp.decode_qk_prep_plan(kv, b.append_layout, b.q_in, b.k_in, b.v_in, b.q_norm_w, b.k_norm_w, b.q,
+                                       None, b.workspace)
+            else:
+                rp.decode_qk_prep(kv, b.append_layout, b.q_in, b.k_in, b.v_in, b.q_norm_w, b.k_norm_w, b.q, None)
             rp.attn_parts(kv, b.attn_layout, b.q, b.softmax_scale, b.workspace)
             rp.combine_parts(kv, b.attn_layout, b.out, b.lse, b.workspace)
 
@@ -410,8 +414,8 @@ def fgd_bench(args):
     the live batch is 16 sequences. Each group has a 512-token prompt; the
     responses are uniform in [0, 6016], about 3.5k tokens of context per
     sequence on average. Qwen3-1.7B layer shape, bf16 KV. A step starts from
-    the raw projections: q/k RMS norm and rotary embedding with the k/v append,
-    then the plan, the partial results and the combine.
+    the raw projections: q/k RMS norm and rotary embedding with the k/v append
+    and the plan (one launch), then the partial results and the combine.
     """
     import numpy as np
     import torch
@@ -432,8 +436,9 @@ def fgd_bench(args):
     bm = byte_model(wl)
     prep_extra = 2 * S * wl.num_q_heads * wl.head_dim * 2      # raw q read and prepared q written
     total = bm["total"] + prep_extra
-    stages = ["prep", "plan", "parts", "combine"]
-    calls = {"prep": b.qk_prep, "plan": b.plan, "parts": b.attn_parts, "combine": b.combine_parts}
+    # rp_decode_qk_prep_plan: the prep and the plan of the step in one launch.
+    stages = ["prep+plan", "parts", "combine"]
+    calls = {"prep+plan": b.qk_prep_plan, "parts": b.attn_parts, "combine": b.combine_parts}
 
     def step(evs=None):
         for i, name in enumerate(stages):

@@ -155,6 +155,24 @@ rp_status rp_decode_qk_prep(const rp_paged_kv* kv, const rp_group_layout* layout
                             double rms_eps, double rope_theta,
                             void* q_out, void* k_out, hipStream_t stream);
 
+/* rp_decode_qk_prep followed by rp_plan for the attention over the advanced
+ * lengths, as one call: the q/k prep and append exactly as rp_decode_qk_prep
+ * with `layout` (resp_lens = the tokens already cached), and the work plan
+ * of rp_plan for the same batch with resp_lens[s] + 1 response tokens, in
+ * `workspace` (at least rp_group_decode_attn_workspace_size bytes of this
+ * layout, 256-byte aligned). Then rp_attn_parts and rp_combine_parts with
+ * the advanced layout (the same arrays, resp_lens + 1) complete the decode
+ * step. Batches of at most 64 sequences (the frontier batches of
+ * frontier-group dispatch, Section 3.3: F_w groups of K samples) take one
+ * launch, the plan built by one wave beside the prep blocks; larger ones
+ * take the two launches. Same arguments, checks and errors as the two calls. */
+rp_status rp_decode_qk_prep_plan(const rp_paged_kv* kv, const rp_group_layout* layout,
+                                 const void* q_in, const void* k_in, const void* v_in,
+                                 const void* q_norm_w, const void* k_norm_w,
+                                 double rms_eps, double rope_theta,
+                                 void* q_out, void* k_out,
+                                 void* workspace, size_t workspace_bytes, hipStream_t stream);
+
 /* Workspace bytes needed by rp_group_decode_attn / rp_plan for this shape.
  * Depends only on host-side scalars (S, num_groups, Hq, Hkv, head_dim,
  * max_prefix_pages, max_resp_pages); *bytes is a host pointer. */

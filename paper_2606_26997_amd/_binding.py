@@ -30,7 +30,7 @@ EXPORTED = ("rp_status_string", "rp_last_error", "rp_kv_append",
             "rp_group_decode_attn_workspace_size", "rp_group_decode_attn", "rp_lse_combine",
             "rp_plan", "rp_attn_parts", "rp_combine_parts", "rp_plan_layout", "rp_validate_layout",
             "rp_prefill_kv_write", "rp_prefill_attn", "rp_decode_qk_prep", "rp_sched_simulate",
-            "rp_grpo_advantage", "rp_prefill", "rp_group_decode_attn_noalloc")
+            "rp_grpo_advantage", "rp_prefill", "rp_group_decode_attn_noalloc", "rp_decode_qk_prep_plan")
 RP_SCHED_MODES = {"slime": 0, "cgp": 1, "cgp_fgd": 2}
 
 
@@ -113,6 +113,8 @@ def load() -> ctypes.CDLL:
         "rp_prefill_attn": (ctypes.c_int, [P, P, P, P, P, F32, P, P, P]),
         "rp_prefill": (ctypes.c_int, [P, P, P, P, P, F32, P, P, P]),
         "rp_decode_qk_prep": (ctypes.c_int, [P, P, P, P, P, P, P, ctypes.c_double, ctypes.c_double, P, P, P]),
+        "rp_decode_qk_prep_plan": (ctypes.c_int, [P, P, P, P, P, P, P, ctypes.c_double, ctypes.c_double, P, P, P,
+                                                   ctypes.c_size_t, P]),
         "rp_sched_simulate": (ctypes.c_int, [P, P, P, P, P, P, P, P, P, P]),
         "rp_grpo_advantage": (ctypes.c_int, [P, I32, I32, ctypes.c_double, I32, P, P, P, P]),
     }
@@ -187,6 +189,17 @@ def decode_qk_prep(kv, layout, q_in, k_in, v_in, q_norm_w, k_norm_w, q_out, k_ou
                                     _ptr(q_norm_w), _ptr(k_norm_w), float(rms_eps), float(rope_theta),
                                     _ptr(q_out), _ptr(k_out), _stream(stream)),
            "rp_decode_qk_prep")
+
+
+def decode_qk_prep_plan(kv, layout, q_in, k_in, v_in, q_norm_w, k_norm_w, q_out, k_out, workspace, *,
+                        rms_eps=1e-6, rope_theta=1e6, stream=None) -> None:
+    """q/k prep with the append (``layout``: pre-append lengths) and the plan of the attention over the
+    advanced lengths, in ``workspace``."""
+    _check(load().rp_decode_qk_prep_plan(ctypes.byref(kv), ctypes.byref(layout), _ptr(q_in), _ptr(k_in),
+                                         _ptr(v_in), _ptr(q_norm_w), _ptr(k_norm_w), float(rms_eps),
+                                         float(rope_theta), _ptr(q_out), _ptr(k_out), _ptr(workspace),
+                                         _ws_bytes(workspace), _stream(stream)),
+           "rp_decode_qk_prep_plan")
 
 
 def grpo_advantage(rewards, advantages, group_mean=None, group_std=None, *, eps_std=1e-6, ddof=1,

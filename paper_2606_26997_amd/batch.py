@@ -118,6 +118,13 @@ class DeviceBatch:
         self.qk_prep(stream)
         self.attention(stream)
 
+    def qk_prep_plan(self, stream=None):
+        """``qk_prep`` and the plan of the attention over the advanced lengths (one launch for small
+        batches); ``attn_parts`` and ``combine_parts`` then finish the step."""
+        B.decode_qk_prep_plan(self.kv, self.append_layout, self.q_in, self.k_in, self.v_in, self.q_norm_w,
+                              self.k_norm_w, self.q, self.k_out, self.workspace, rms_eps=self.rms_eps,
+                              rope_theta=self.rope_theta, stream=stream)
+
     # -- staged form ------------------------------------------------------------
     def plan(self, stream=None):
         B.plan(self.kv, self.attn_layout, self.workspace, stream)

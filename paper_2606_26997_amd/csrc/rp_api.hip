@@ -239,6 +239,71 @@ rp::AttnArgs attn_args(const rp_paged_kv* kv, const rp_group_layout* l, const vo
   return a;
 }
 
+// The planner's arguments for a prepared batch (queries the device's compute
+// units, which set the piece length).
+rp_status plan_args(const Shape& sh, const rp_group_layout* l, void* ws, const WsLayout& w, int len_add,
+                    rp::PlanArgs* a) {
+  int cus = 0;
+  rp_status st = device_cus(&cus);
+  if (st != RP_OK) return st;
+  a->num_seqs = sh.S;
+  a->num_groups = sh.G;
+  a->num_q_heads = sh.Hq;
+  a->num_kv_heads = sh.Hkv;
+  a->num_cus = cus;
+  a->seq_to_group = l->seq_to_group;
+  a->prefix_lens = l->prefix_lens;
+  a->resp_lens = l->resp_lens;
+  a->len_add = len_add;
+  a->max_prefix_pages = sh.max_pp;
+  a->max_resp_pages = sh.max_rp;
+  a->view = plan_view(ws, w);
+  return RP_OK;
+}
+
+// Checks and launch arguments of the decode step's q/k prep.
+rp_status qk_prep_args(const rp_paged_kv* kv, const rp_group_layout* l, const Shape& sh, const void* q_in,
+                       const void* k_in, const void* v_in, const void* q_norm_w, const void* k_norm_w,
+                       double rms_eps, double rope_theta, void* q_out, void* k_out, rp::QkPrepArgs* a) {
+  if (!(rms_eps >= 0.0) || !std::isfinite(rms_eps)) return fail(RP_ERR_INVALID_ARG, "rms_eps must be finite and >= 0");
+  if (!(rope_theta > 0.0) || !std::isfinite(rope_theta))
+    return fail(RP_ERR_INVALID_ARG, "rope_theta must be finite and > 0");
+  if (sh.S == 0) return RP_OK;
+  const void* in[] = {q_in, k_in, v_in, q_norm_w, k_norm_w, q_out};
+  for (const void* p : in)
+    if (p == nullptr || !aligned(p, 16))
+      return fail(RP_ERR_INVALID_ARG, "q_in/k_in/v_in/q_norm_w/k_norm_w/q_out must be non-NULL and 16-byte aligned");
+  if (k_out != nullptr && !aligned(k_out, 16)) return fail(RP_ERR_INVALID_ARG, "k_out must be 16-byte aligned");
+  if (sh.max_rp < 1) return fail(RP_ERR_INVALID_ARG, "max_resp_pages must be >= 1 to append");
+  a->k_pages = kv->k_pages;
+  a->v_pages = kv->v_pages;
+  a->k_scale = kv->k_scale;
+  a->v_scale = kv->v_scale;
+  a->num_pages = kv->num_pages;
+  a->num_kv_heads = sh.Hkv;
+  a->num_q_heads = sh.Hq;
+  a->num_seqs = sh.S;
+  a->num_groups = sh.G;
+  a->seq_to_group = l->seq_to_group;
+  a->prefix_lens = l->prefix_lens;
+  a->resp_lens = l->resp_lens;
+  a->resp_block_table = l->resp_block_table;
+  a->max_resp_pages = sh.max_rp;
+  a->q_in = static_cast<const uint16_t*>(q_in);
+  a->k_in = static_cast<const uint16_t*>(k_in);
+  a->v_in = static_cast<const uint16_t*>(v_in);
+  a->q_norm_w = static_cast<const uint16_t*>(q_norm_w);
+  a->k_norm_w = static_cast<const uint16_t*>(k_norm_w);
+  a->rms_eps = rms_eps;
+  // Rotary frequencies on the host in fp64 (libm pow), passed with the arguments.
+  for (int i = 0; i < rp::kMaxHeadDim / 2; ++i)
+    a->inv_freq[i] = i < sh.D / 2 ? std::pow(rope_theta, (-2.0 * i) / sh.D) : 0.0;
+  a->q_out = static_cast<uint16_t*>(q_out);
+  a->k_out = static_cast<uint16_t*>(k_out);
+  a->blocks_per_seq = 0;
+  return RP_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -277,21 +342,9 @@ rp_status rp_plan(const rp_paged_kv* kv, const rp_group_layout* l, void* ws, siz
   WsLayout w;
   rp_status st = prepare(kv, l, ws, ws_bytes, &sh, &w);
   if (st != RP_OK || sh.S == 0) return st;
-  int cus = 0;
-  st = device_cus(&cus);
-  if (st != RP_OK) return st;
   rp::PlanArgs a;
-  a.num_seqs = sh.S;
-  a.num_groups = sh.G;
-  a.num_q_heads = sh.Hq;
-  a.num_kv_heads = sh.Hkv;
-  a.num_cus = cus;
-  a.seq_to_group = l->seq_to_group;
-  a.prefix_lens = l->prefix_lens;
-  a.resp_lens = l->resp_lens;
-  a.max_prefix_pages = sh.max_pp;
-  a.max_resp_pages = sh.max_rp;
-  a.view = plan_view(ws, w);
+  st = plan_args(sh, l, ws, w, 0, &a);
+  if (st != RP_OK) return st;
   hipError_t e = rp::launch_plan(a, stream);
   return e == hipSuccess ? RP_OK : hip_fail(e, "plan kernel launch");
 }
@@ -430,45 +483,37 @@ rp_status rp_decode_qk_prep(const rp_paged_kv* kv, const rp_group_layout* l, con
   Shape sh;
   rp_status st = check_shape(kv, l, &sh);
   if (st != RP_OK) return st;
-  if (!(rms_eps >= 0.0) || !std::isfinite(rms_eps)) return fail(RP_ERR_INVALID_ARG, "rms_eps must be finite and >= 0");
-  if (!(rope_theta > 0.0) || !std::isfinite(rope_theta))
-    return fail(RP_ERR_INVALID_ARG, "rope_theta must be finite and > 0");
-  if (sh.S == 0) return RP_OK;
-  const void* in[] = {q_in, k_in, v_in, q_norm_w, k_norm_w, q_out};
-  for (const void* p : in)
-    if (p == nullptr || !aligned(p, 16))
-      return fail(RP_ERR_INVALID_ARG, "q_in/k_in/v_in/q_norm_w/k_norm_w/q_out must be non-NULL and 16-byte aligned");
-  if (k_out != nullptr && !aligned(k_out, 16)) return fail(RP_ERR_INVALID_ARG, "k_out must be 16-byte aligned");
-  if (sh.max_rp < 1) return fail(RP_ERR_INVALID_ARG, "max_resp_pages must be >= 1 to append");
   rp::QkPrepArgs a;
-  a.k_pages = kv->k_pages;
-  a.v_pages = kv->v_pages;
-  a.k_scale = kv->k_scale;
-  a.v_scale = kv->v_scale;
-  a.num_pages = kv->num_pages;
-  a.num_kv_heads = sh.Hkv;
-  a.num_q_heads = sh.Hq;
-  a.num_seqs = sh.S;
-  a.num_groups = sh.G;
-  a.seq_to_group = l->seq_to_group;
-  a.prefix_lens = l->prefix_lens;
-  a.resp_lens = l->resp_lens;
-  a.resp_block_table = l->resp_block_table;
-  a.max_resp_pages = sh.max_rp;
-  a.q_in = static_cast<const uint16_t*>(q_in);
-  a.k_in = static_cast<const uint16_t*>(k_in);
-  a.v_in = static_cast<const uint16_t*>(v_in);
-  a.q_norm_w = static_cast<const uint16_t*>(q_norm_w);
-  a.k_norm_w = static_cast<const uint16_t*>(k_norm_w);
-  a.rms_eps = rms_eps;
-  // Rotary frequencies on the host in fp64 (libm pow), passed with the arguments.
-  for (int i = 0; i < rp::kMaxHeadDim / 2; ++i)
-    a.inv_freq[i] = i < sh.D / 2 ? std::pow(rope_theta, (-2.0 * i) / sh.D) : 0.0;
-  a.q_out = static_cast<uint16_t*>(q_out);
-  a.k_out = static_cast<uint16_t*>(k_out);
-  a.blocks_per_seq = 0;
+  st = qk_prep_args(kv, l, sh, q_in, k_in, v_in, q_norm_w, k_norm_w, rms_eps, rope_theta, q_out, k_out, &a);
+  if (st != RP_OK || sh.S == 0) return st;
   hipError_t e = rp::launch_qk_prep(a, sh.D, sh.fp8, stream);
   return e == hipSuccess ? RP_OK : hip_fail(e, "decode q/k prep kernel launch");
+}
+
+rp_status rp_decode_qk_prep_plan(const rp_paged_kv* kv, const rp_group_layout* l, const void* q_in,
+                                 const void* k_in, const void* v_in, const void* q_norm_w, const void* k_norm_w,
+                                 double rms_eps, double rope_theta, void* q_out, void* k_out, void* ws,
+                                 size_t ws_bytes, hipStream_t stream) {
+  g_err[0] = 0;
+  Shape sh;
+  WsLayout w;
+  rp_status st = prepare(kv, l, ws, ws_bytes, &sh, &w);
+  if (st != RP_OK) return st;
+  rp::QkPrepArgs a;
+  st = qk_prep_args(kv, l, sh, q_in, k_in, v_in, q_norm_w, k_norm_w, rms_eps, rope_theta, q_out, k_out, &a);
+  if (st != RP_OK || sh.S == 0) return st;
+  rp::PlanArgs p;
+  st = plan_args(sh, l, ws, w, 1, &p);
+  if (st != RP_OK) return st;
+  hipError_t e;
+  if (sh.S <= rp::kSmallPlanMaxSeqs && sh.G <= rp::kPlanMaxGroups) {
+    e = rp::launch_qk_prep_plan(a, p, sh.D, sh.fp8, stream);
+    return e == hipSuccess ? RP_OK : hip_fail(e, "decode q/k prep + plan kernel launch");
+  }
+  e = rp::launch_qk_prep(a, sh.D, sh.fp8, stream);
+  if (e != hipSuccess) return hip_fail(e, "decode q/k prep kernel launch");
+  e = rp::launch_plan(p, stream);
+  return e == hipSuccess ? RP_OK : hip_fail(e, "plan kernel launch");
 }
 
 rp_status rp_grpo_advantage(const float* rewards, int32_t num_groups, int32_t group_size, double eps_std,

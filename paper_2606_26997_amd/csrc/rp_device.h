@@ -52,6 +52,8 @@ enum : int {
 };
 // Largest group count the planner keeps in LDS.
 constexpr int kPlanMaxGroups = 4096;
+// Batches of at most this many sequences are planned by a single wave.
+constexpr int kSmallPlanMaxSeqs = 64;
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));

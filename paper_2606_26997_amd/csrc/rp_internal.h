@@ -30,6 +30,7 @@ struct PlanArgs {
   const int* seq_to_group;
   const int* prefix_lens;
   const int* resp_lens;
+  int len_add;  // the plan is for resp_lens[s] + len_add response tokens (1: after this step's append)
   int max_prefix_pages, max_resp_pages;
   PlanView view;
 };
@@ -152,6 +153,9 @@ struct ValidateArgs {
 };
 
 hipError_t launch_plan(const PlanArgs& a, hipStream_t stream);
+// q/k prep and the plan of the attention after its append in one launch
+// (batches of at most 64 sequences; the plan's len_add is 1).
+hipError_t launch_qk_prep_plan(QkPrepArgs a, const PlanArgs& p, int head_dim, bool fp8, hipStream_t stream);
 // Grid sizes are upper bounds from host scalars; idle waves exit at once.
 hipError_t launch_attn_parts(const AttnArgs& a, int head_dim, int n_rep, bool fp8, long long max_prefix_items,
                              long long max_resp_items, hipStream_t stream);

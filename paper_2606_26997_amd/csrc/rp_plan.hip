@@ -10,15 +10,16 @@
 // the wave totals.
 #include "rp_device.h"
 #include "rp_internal.h"
+#include "rp_plan_small.h"
 
 namespace rp {
 namespace {
 
 // The planner runs as one workgroup: 1024 threads in general, four waves for
-// batches of at most kMediumPlanSeqs sequences and one wave for at most
-// kSmallPlanSeqs (fewer waves to meet at each barrier, and a smaller launch
-// starts sooner; measured).
-constexpr int kSmallPlanSeqs = 64;
+// batches of at most kMediumPlanSeqs sequences (fewer waves to meet at each
+// barrier, and a smaller launch starts sooner; measured). Batches of at most
+// kSmallPlanMaxSeqs sequences take the single-wave planner of
+// rp_plan_small.h.
 constexpr int kMediumPlanSeqs = 256;
 
 __device__ inline long long wave_incl_scan(long long v, int lane) {
@@ -103,7 +104,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
   unsigned long long my_pages = 0;
   for (int s = t; s < S; s += kPlanThreads) {
     const int g = clamp_group(a.seq_to_group[s], G);
-    const int L = clamp_len(a.resp_lens[s], a.max_resp_pages);
+    const int L = plan_resp_len(a, s);
     if (s < kPlanSeqBlock) {
       s_sg[s] = g;
       s_sl[s] = L;
@@ -117,19 +118,15 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
   __syncthreads();
   // B: the multiple of kRespChunkStep nearest to W / (kRespChunkStep * target
   // units), W = response pages x kv-heads, clamped to the candidates.
-  const long long W = (long long)s_pages * a.num_kv_heads;
-  const long long unit = (long long)kRespChunkStep * kUnitsPerCu * max(a.num_cus, 1);
-  int chunk = kRespChunkStep * (int)min(max((W + unit / 2) / unit, 1ll), (long long)kRespChunkChoices);
   // Below three quarters of one step, 16-page pieces if every response fits
   // the workspace's partial-result slots at that length.
-  if (4 * W < 3 * unit && v.max_resp_chunks >= cdiv(a.max_resp_pages, kRespChunkPagesSmall))
-    chunk = kRespChunkPagesSmall;
+  const int chunk = plan_piece_pages(a, (long long)s_pages * a.num_kv_heads);
 
   // Second pass (lengths from LDS where the first pass kept them): B-sized
   // pieces and the ragged pieces per page count.
   int my_big = 0;
   for (int s = t; s < S; s += kPlanThreads) {
-    const int L = s < kPlanSeqBlock ? s_sl[s] : clamp_len(a.resp_lens[s], a.max_resp_pages);
+    const int L = s < kPlanSeqBlock ? s_sl[s] : plan_resp_len(a, s);
     const int pages = cdiv(L, kPage);
     my_big += pages / chunk;
     if (pages % chunk) atomicAdd(&s_hist[pages % chunk], 1);
@@ -194,7 +191,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
       __syncthreads();  // the previous pass is done with the LDS copies
       for (int k = t; k < n; k += kPlanThreads) {
         s_sg[k] = clamp_group(a.seq_to_group[base + k], G);
-        s_sl[k] = clamp_len(a.resp_lens[base + k], a.max_resp_pages);
+        s_sl[k] = plan_resp_len(a, base + k);
       }
       __syncthreads();
     }
@@ -267,10 +264,15 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
   }
 }
 
+__global__ __launch_bounds__(64) void plan_small_kernel(PlanArgs a) {
+  __shared__ int s_cnt[kPlanMaxGroups];
+  plan_small(a, s_cnt);
+}
+
 }  // namespace
 
 hipError_t launch_plan(const PlanArgs& a, hipStream_t stream) {
-  if (a.num_seqs <= kSmallPlanSeqs) plan_kernel<64, 256><<<1, 64, 0, stream>>>(a);
+  if (a.num_seqs <= kSmallPlanMaxSeqs) plan_small_kernel<<<1, 64, 0, stream>>>(a);
   else if (a.num_seqs <= kMediumPlanSeqs) plan_kernel<256, 1024><<<1, 256, 0, stream>>>(a);
   else plan_kernel<1024, 4096><<<1, 1024, 0, stream>>>(a);
   return hipGetLastError();

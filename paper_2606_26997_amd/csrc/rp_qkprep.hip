@@ -20,6 +20,7 @@
 // once, folded with the norm weights into LDS tables.
 #include "rp_device.h"
 #include "rp_internal.h"
+#include "rp_plan_small.h"
 
 namespace rp {
 namespace {
@@ -163,18 +164,21 @@ __device__ inline void prep_slot(const QkPrepArgs& a, int s, int kind, int head,
   }
 }
 
+// Per pair i and weight set (0: q, 1: k): A = w[i] cos, B = w[i + D/2] sin,
+// C = w[i + D/2] cos, E = w[i] sin, so that with the norm factor inv
+//   out[i] = inv (x[i] A - x[i + D/2] B),  out[i + D/2] = inv (x[i + D/2] C + x[i] E).
+template <int D>
+using PrepTables = double[2][4][D / 2];
+
+// Block `bid` of the prep grid (blocks_per_seq blocks per sequence).
 template <int D, bool FP8, int SPL>
-__global__ __launch_bounds__(kPrepThreads) void qk_prep_kernel(const QkPrepArgs a) {
+__device__ __forceinline__ void prep_block(const QkPrepArgs& a, int bid, PrepTables<D>& s_tab) {
   constexpr int W = D / 64;
   constexpr int HALF = D / 2;
-  // Per pair i and weight set (0: q, 1: k): A = w[i] cos, B = w[i + D/2] sin,
-  // C = w[i + D/2] cos, E = w[i] sin, so that with the norm factor inv
-  //   out[i] = inv (x[i] A - x[i + D/2] B),  out[i + D/2] = inv (x[i + D/2] C + x[i] E).
-  __shared__ double s_tab[2][4][HALF];
   const int Hq = a.num_q_heads, Hkv = a.num_kv_heads;
   const int t = threadIdx.x, l16 = t & (kSlotLanes - 1);
-  const int s = blockIdx.x / a.blocks_per_seq;
-  const int slot0 = (blockIdx.x - s * a.blocks_per_seq) * (kGroups * SPL) + t / kSlotLanes;
+  const int s = bid / a.blocks_per_seq;
+  const int slot0 = (bid - s * a.blocks_per_seq) * (kGroups * SPL) + t / kSlotLanes;
   const int c1 = l16 * (D / 32), c2 = HALF + l16 * (D / 32);
   const int g = clamp_group(a.seq_to_group[s], a.num_groups);
   const int L = a.resp_lens[s];
@@ -217,6 +221,29 @@ __global__ __launch_bounds__(kPrepThreads) void qk_prep_kernel(const QkPrepArgs 
   }
 }
 
+template <int D, bool FP8, int SPL>
+__global__ __launch_bounds__(kPrepThreads) void qk_prep_kernel(const QkPrepArgs a) {
+  __shared__ PrepTables<D> s_tab;
+  prep_block<D, FP8, SPL>(a, blockIdx.x, s_tab);
+}
+
+// The prep of a small batch and the plan of the attention that follows, in
+// one launch: the first workgroup's first wave builds the plan (the planner
+// of rp_plan_small.h; the workgroup's other waves have nothing to do), every
+// other workgroup is a prep block. The two share no data.
+template <int D, bool FP8>
+__global__ __launch_bounds__(kPrepThreads) void qk_prep_plan_kernel(const QkPrepArgs a, const PlanArgs p) {
+  __shared__ union {
+    PrepTables<D> tab;
+    int cnt[kPlanMaxGroups];
+  } sm;
+  if (blockIdx.x == 0) {
+    if (threadIdx.x < 64) plan_small(p, sm.cnt);
+    return;
+  }
+  prep_block<D, FP8, 1>(a, blockIdx.x - 1, sm.tab);
+}
+
 template <int D, int SPL>
 hipError_t launch_d(QkPrepArgs a, bool fp8, hipStream_t stream) {
   a.blocks_per_seq = cdiv(a.num_q_heads + 2 * a.num_kv_heads, kGroups * SPL);
@@ -226,7 +253,24 @@ hipError_t launch_d(QkPrepArgs a, bool fp8, hipStream_t stream) {
   return hipGetLastError();
 }
 
+template <int D>
+hipError_t launch_prep_plan_d(QkPrepArgs a, const PlanArgs& p, bool fp8, hipStream_t stream) {
+  a.blocks_per_seq = cdiv(a.num_q_heads + 2 * a.num_kv_heads, kGroups);
+  const dim3 grid((unsigned)((long long)a.num_seqs * a.blocks_per_seq + 1)), block(kPrepThreads);
+  if (fp8) qk_prep_plan_kernel<D, true><<<grid, block, 0, stream>>>(a, p);
+  else qk_prep_plan_kernel<D, false><<<grid, block, 0, stream>>>(a, p);
+  return hipGetLastError();
+}
+
 }  // namespace
+
+hipError_t launch_qk_prep_plan(QkPrepArgs a, const PlanArgs& p, int head_dim, bool fp8, hipStream_t stream) {
+  if (a.num_seqs <= 0) return hipSuccess;
+  if (a.num_seqs > kSmallPlanMaxSeqs || p.num_seqs != a.num_seqs) return hipErrorInvalidValue;
+  if (head_dim == 128) return launch_prep_plan_d<128>(a, p, fp8, stream);
+  if (head_dim == 64) return launch_prep_plan_d<64>(a, p, fp8, stream);
+  return hipErrorInvalidValue;
+}
 
 // Small batches give each 16-lane group one slot (more blocks in flight);
 // from 1024 sequences on, two slots, so that a block covers 32 slots and

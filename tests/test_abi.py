@@ -297,3 +297,19 @@ def test_noalloc_scratch_limit_and_refusal():
                                             ctypes.c_float(0.1), None, None, None) == rp.RP_OK
     assert lib.rp_group_decode_attn_noalloc(ctypes.byref(_kv(head_dim=96)), ctypes.byref(lay), A,
                                             ctypes.c_float(0.1), A, None, None) == rp.RP_ERR_UNSUPPORTED
+
+
+def test_decode_qk_prep_plan_argument_checks():
+    """The fused prep + plan call checks the prep's arguments and the plan's workspace before any launch."""
+    kv, lay = _kv(), _layout()
+    lib = rp.load()
+    _, need = _ws_size(kv, lay)
+    call = lambda lay_=lay, q=A, eps=1e-6, ws=A, n=need: lib.rp_decode_qk_prep_plan(
+        ctypes.byref(kv), ctypes.byref(lay_), q, A, A, A, A, eps, 1e6, A, None, ws, n, None)
+    assert call(q=None) == rp.RP_ERR_INVALID_ARG and "q_in" in rp.last_error()
+    assert call(eps=-1.0) == rp.RP_ERR_INVALID_ARG and "rms_eps" in rp.last_error()
+    assert call(n=need - 1) == rp.RP_ERR_WORKSPACE
+    assert call(ws=A + 64) == rp.RP_ERR_WORKSPACE
+    assert call(ws=None) == rp.RP_ERR_WORKSPACE
+    assert call(lay_=_layout(mrp=0), n=_ws_size(kv, _layout(mrp=0))[1]) == rp.RP_ERR_INVALID_ARG
+    assert call(lay_=_layout(num_seqs=0), q=None, ws=None, n=0) == rp.RP_OK

@@ -143,6 +143,22 @@ def _case(name):
         G, S = 6, 5
         s2g = np.array([0, 0, 3, 3, 5])
         P, L = np.array([0, 17, 300, 0, 5, 16]), np.array([0, 512, 0, 513, 1])
+    elif name == "small-many-groups":       # single-wave planner, groups beyond the first 64 live
+        G, S = 300, 40
+        s2g = rng.integers(0, G, S)
+        P, L = rng.integers(0, 700, G), rng.integers(0, 2000, S)
+    elif name == "small-equal-lengths":     # 64 sequences in 64 groups, ties among the last pieces
+        G, S = 64, 64
+        s2g = rng.permutation(S)
+        P, L = rng.integers(1, 200, G), np.full(S, 1000)
+    elif name == "single-sequence":
+        G, S = 1, 1
+        s2g = np.zeros(1, int)
+        P, L = np.array([33]), np.array([4097])
+    elif name == "small-all-empty":         # no prefix, no response tokens
+        G, S = 3, 10
+        s2g = rng.integers(0, G, S)
+        P, L = np.zeros(G, int), np.zeros(S, int)
     else:
         raise KeyError(name)
     return G, s2g, P, L
@@ -150,7 +166,8 @@ def _case(name):
 
 CASES = ["qwen-layer-uniform", "lognormal-tail", "frontier-random-map", "long-context", "many-sequences",
          "many-pieces", "frontier-dispatch-16", "frontier-dispatch-64", "frontier-dispatch-64-long",
-         "few-long-sequences", "empty-and-idle-groups"]
+         "few-long-sequences", "empty-and-idle-groups", "small-many-groups", "small-equal-lengths",
+         "single-sequence", "small-all-empty"]
 
 
 @pytest.mark.parametrize("name", CASES)
@@ -162,7 +179,8 @@ def test_plan_matches_its_contract(name):
     B = check_plan(b, s2g, P, L, rbt, G)
     if torch.cuda.get_device_properties(0).multi_processor_count == 256:   # MI355X: every candidate B occurs
         want = {"frontier-dispatch-16": 16, "few-long-sequences": 16, "empty-and-idle-groups": 16,
-                "frontier-dispatch-64": 64, "frontier-dispatch-64-long": 96}.get(name, 128)
+                "frontier-dispatch-64": 64, "frontier-dispatch-64-long": 96, "small-many-groups": 16,
+                "small-equal-lengths": 16, "single-sequence": 16, "small-all-empty": 16}.get(name, 128)
         assert B == want, (name, B)
     # A second plan into the same workspace gives the same B-page items.
     check_plan(b, s2g, P, L, rbt, G)

@@ -232,3 +232,68 @@ def test_decode_step_at_frontier_operating_point(kv_dtype):
     out = b.out.float().cpu().numpy().astype(np.float64)
     lse = b.lse.cpu().numpy().astype(np.float64)
     compare(out, lse, ref_out, ref_lse, kv_dtype, label=f"decode step {kv_dtype}")
+
+
+FUSED = [
+    # name, seq_to_group, prefix_lens, response lengths (seeded draw), Hq, Hkv, d, kv dtype
+    ("frontier-2x8", np.repeat([0, 1], 8), [512, 300], (0, 6017), 16, 8, 128, "bf16"),
+    ("fp8-5", [0, 0, 1, 1, 1], [33, 200], (0, 700), 16, 8, 128, "fp8"),
+    ("d64-64-seqs", np.arange(64) % 5, [16, 0, 77, 130, 3], (0, 900), 8, 2, 64, "bf16"),
+    ("two-launches-100", np.arange(100) // 10, [100] * 10, (0, 1200), 16, 8, 128, "bf16"),
+]
+
+
+@pytest.mark.parametrize("case", FUSED, ids=[c[0] for c in FUSED])
+def test_prep_plan_call_equals_prep_then_plan(case):
+    """rp_decode_qk_prep_plan (one launch up to 64 sequences) leaves the same q, pool bytes and plan as
+    rp_decode_qk_prep followed by rp_plan over the advanced lengths; attention on that plan matches the
+    pure oracle's decode step."""
+    name, s2g, P, (lo, hi), Hq, Hkv, d, dt = case
+    _say(f"prep+plan {name}")
+    rng = np.random.default_rng(len(name))
+    R = rng.integers(lo, hi, len(s2g))
+    wl, x, ref = _setup(s2g, P, R, Hq, Hkv, d, dt, seed=len(name) * 3)
+    import paper_2606_26997_amd as rp
+    one = rp.DeviceBatch.from_workload(wl)
+    for b in (ref, one):
+        b.set_projections(x.q_in, x.k_in, x.v_in, x.q_norm_w, x.k_norm_w, keep_k=True)
+    ref.qk_prep()
+    ref.plan()
+    one.workspace.fill_(255)
+    one.qk_prep_plan()
+    torch.cuda.synchronize()
+    assert np.array_equal(_bits(one.q), _bits(ref.q)) and np.array_equal(_bits(one.k_out), _bits(ref.k_out))
+    for g, r in zip(_pool_bytes(one, dt), _pool_bytes(ref, dt)):
+        assert np.array_equal(g, r), name
+    p1, p2 = one.plan_contents(), ref.plan_contents()
+    assert np.array_equal(p1["hdr"][:4], p2["hdr"][:4]), name          # the header's used slots
+    for key in ("grp_off", "prefix_items", "seq_parts"):
+        assert np.array_equal(p1[key], p2[key]), (name, key)
+    # Members within a group, and last pieces of equal size, may come in any order (the plan contract).
+    off = p1["grp_off"]
+    for g in range(len(off) - 1):
+        assert sorted(p1["grp_members"][off[g]:off[g + 1]]) == sorted(p2["grp_members"][off[g]:off[g + 1]])
+    nb = int(p1["hdr"][2])
+    assert np.array_equal(p1["resp_items"][:nb], p2["resp_items"][:nb]), name
+    assert sorted(map(tuple, p1["resp_items"][nb:])) == sorted(map(tuple, p2["resp_items"][nb:])), name
+    for b in (ref, one):
+        b.attn_parts()
+        b.combine_parts()
+    torch.cuda.synchronize()
+    # Same pieces, so the same partial results and the same merge: bit for bit.
+    assert torch.equal(one.out.view(torch.int16), ref.out.view(torch.int16))
+    assert torch.equal(one.lse.view(torch.int32), ref.lse.view(torch.int32))
+    qb, _, pool = oracle.decode_step_prep(q_in=x.q_in, k_in=x.k_in, v_in=x.v_in, q_norm_w=x.q_norm_w,
+                                          k_norm_w=x.k_norm_w, k_pages=wl.k_pages, v_pages=wl.v_pages,
+                                          k_scale=wl.k_scale, v_scale=wl.v_scale, kv_dtype=dt, page_size=16,
+                                          seq_to_group=wl.seq_to_group, prefix_lens=wl.prefix_lens,
+                                          resp_lens=wl.resp_lens, resp_block_table=wl.resp_block_table)
+    kp, vp, ks, vs = pool
+    ref_out, ref_lse = oracle.decode_attention(k_pages=kp, v_pages=vp, k_scale=ks, v_scale=vs, kv_dtype=dt,
+                                               page_size=16, seq_to_group=wl.seq_to_group,
+                                               prefix_lens=wl.prefix_lens, prefix_block_table=wl.prefix_block_table,
+                                               resp_lens=wl.resp_lens + 1, resp_block_table=wl.resp_block_table,
+                                               q=qb, softmax_scale=wl.softmax_scale)
+    out = one.out.float().cpu().numpy().astype(np.float64)
+    lse = one.lse.cpu().numpy().astype(np.float64)
+    compare(out, lse, ref_out, ref_lse, dt, label=f"prep+plan {name}")
