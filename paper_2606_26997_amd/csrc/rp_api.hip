@@ -562,8 +562,10 @@ static rp_status prefill_args(const rp_paged_kv* kv, const rp_prefill_layout* l,
     if (l->max_prefix_pages < 1 || l->prefix_block_table == nullptr)
       return fail(RP_ERR_INVALID_ARG, "prefix_block_table must be non-NULL with max_prefix_pages >= 1");
   }
+  // One prompt's K/V rows are addressed with 32-bit byte offsets.
   if ((long long)l->num_groups * l->max_prefix_pages * kv->num_kv_heads >= (1ll << 31) ||
-      (long long)l->num_tokens * l->num_q_heads * kv->head_dim >= (1ll << 40))
+      (long long)l->num_tokens * l->num_q_heads * kv->head_dim >= (1ll << 40) ||
+      (long long)l->max_prefix_pages * rp::kPage * kv->num_kv_heads * kv->head_dim * 2 >= (1ll << 32))
     return fail(RP_ERR_UNSUPPORTED, "prefill too large");
   a->k_pages = kv->k_pages;
   a->v_pages = kv->v_pages;

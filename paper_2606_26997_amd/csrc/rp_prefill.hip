@@ -148,22 +148,27 @@ struct PfBlock {
   u32x4_t k0, k1, v0, v1;
 };
 
+// Byte offsets within one prompt's rows fit 32 bits (the host checks it), so
+// the loads take the group's wave-uniform base plus a 32-bit offset: no
+// 64-bit address arithmetic per block.
 template <int D>
-__device__ inline void pf_load(const uint16_t* kbase, const uint16_t* vbase, size_t pitch, int u0, int last, int t,
+__device__ inline void pf_load(const uint16_t* kbase, const uint16_t* vbase, uint32_t pitch, int u0, int last, int t,
                                PfBlock& r) {
   using L = PfSmem<D>;
+  const char* kb = reinterpret_cast<const char*>(kbase);
+  const char* vb = reinterpret_cast<const char*>(vbase);
   {
     const int key = t / (D / 8), col = (t - key * (D / 8)) * 8;
-    const size_t off = (size_t)min(u0 + key, last) * pitch + col;
-    r.k0 = *reinterpret_cast<const u32x4_t*>(kbase + off);
-    r.v0 = *reinterpret_cast<const u32x4_t*>(vbase + off);
+    const uint32_t off = ((uint32_t)min(u0 + key, last) * pitch + (uint32_t)col) * 2u;
+    r.k0 = *reinterpret_cast<const u32x4_t*>(kb + off);
+    r.v0 = *reinterpret_cast<const u32x4_t*>(vb + off);
   }
   if constexpr (L::kPerThread == 2) {
     const int c = t + kPfThreads;
     const int key = c / (D / 8), col = (c - key * (D / 8)) * 8;
-    const size_t off = (size_t)min(u0 + key, last) * pitch + col;
-    r.k1 = *reinterpret_cast<const u32x4_t*>(kbase + off);
-    r.v1 = *reinterpret_cast<const u32x4_t*>(vbase + off);
+    const uint32_t off = ((uint32_t)min(u0 + key, last) * pitch + (uint32_t)col) * 2u;
+    r.k1 = *reinterpret_cast<const u32x4_t*>(kb + off);
+    r.v1 = *reinterpret_cast<const u32x4_t*>(vb + off);
   }
 }
 
@@ -376,12 +381,12 @@ void prefill_attn_kernel(const PrefillArgs a, int max_blocks) {
   // With write_pages, key block b's rows go to the pages from the workgroup
   // whose rows hold token 32 b (every block of the prompt has exactly one).
   PfBlock nx;
-  pf_load<D>(kbase, vbase, kpitch, 0, last, t, nx);
+  pf_load<D>(kbase, vbase, (uint32_t)kpitch, 0, last, t, nx);
   pf_store<D>(smem, t, nx);
   if (WP && T0 == 0) pf_write_pages<D>(a, g, h, 0, last, t, nx);
   __syncthreads();
   for (int blk = 0; blk < nblk; ++blk) {
-    pf_load<D>(kbase, vbase, kpitch, (blk + 1) * kKeyBlk, last, t, nx);
+    pf_load<D>(kbase, vbase, (uint32_t)kpitch, (blk + 1) * kKeyBlk, last, t, nx);
     // Blocks wholly below the diagonal for every (valid) row of the wave skip the mask.
     if ((blk + 1) * kKeyBlk - 1 <= w_first && w_last <= last)
       pf_compute<D, NREP, RT, false>(smem + (blk & 1) * L::kStage, blk * kKeyBlk, last, a.qk_scale, r16, quad, tr,

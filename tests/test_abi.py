@@ -189,6 +189,9 @@ def _prefill_layout(**kw):
 
 
 @pytest.mark.parametrize("lay_kw,status,needle", [
+    # One prompt's rows are addressed with 32-bit byte offsets: 2^20 pages x 16 tokens x 2 kv-heads x 64
+    # x 2 B = 2^32 bytes is one too many.
+    (dict(mpp=1 << 20), rp.RP_ERR_UNSUPPORTED, "too large"),
     (dict(num_q_heads=3), rp.RP_ERR_INVALID_ARG, "multiple"),
     (dict(num_q_heads=6), rp.RP_ERR_UNSUPPORTED, "ratio"),
     (dict(offs=None), rp.RP_ERR_INVALID_ARG, "prompt_offs"),
