@@ -14,8 +14,6 @@ namespace {
 constexpr int kCombineWaves = 4;
 constexpr int kBatch = 8;
 
-// Parts base + b * PPI + slot of the row, for those below `n` (the others
-// read as empty: lse -inf, o 0).
 template <int D>
 __device__ inline void load_batch(const CombineArgs& a, int p0, int n, int base, int slot, int sub, float* lp,
                                   float4* ov) {
@@ -28,17 +26,6 @@ __device__ inline void load_batch(const CombineArgs& a, int p0, int n, int base,
     if (k < n) {
       lp[b] = a.lse_parts[p0 + k];
       ov[b] = *reinterpret_cast<const float4*>(a.o_parts + (size_t)(p0 + k) * D + sub * 4);
-    }
-  }
-}
-
-// Parts below `n` keep their loaded values; the rest become empty.
-__device__ inline void mask_batch(int n, int slot, int ppi, float* lp, float4* ov) {
-#pragma unroll
-  for (int b = 0; b < kBatch; ++b) {
-    if (b * ppi + slot >= n) {
-      lp[b] = -INFINITY;
-      ov[b] = make_float4(0.f, 0.f, 0.f, 0.f);
     }
   }
 }
@@ -66,21 +53,17 @@ __global__ __launch_bounds__(64 * kCombineWaves) void combine_kernel(const Combi
   const int slot = lane / LPP, sub = lane - slot * LPP;
 
   int p0, n;
-  float lp[kBatch];
-  float4 ov[kBatch];
   if (a.row_offs != nullptr) {
     p0 = a.row_offs[row];
     n = a.row_offs[row + 1] - p0;
-    load_batch<D>(a, p0, n, 0, slot, sub, lp, ov);
   } else {
-    // Planned slots: the row's parts start at a known slot, so the first
-    // batch is requested together with the part count (every slot of the
-    // row lies inside the workspace) and masked once the count is known.
-    p0 = row * a.parts_per_row;
-    load_batch<D>(a, p0, a.parts_per_row, 0, slot, sub, lp, ov);
     n = min(max(a.seq_parts[row / a.num_q_heads], 0), a.parts_per_row);
-    mask_batch(n, slot, PPI, lp, ov);
+    p0 = row * a.parts_per_row;
   }
+
+  float lp[kBatch];
+  float4 ov[kBatch];
+  load_batch<D>(a, p0, n, 0, slot, sub, lp, ov);
   float mx = -INFINITY;
 #pragma unroll
   for (int b = 0; b < kBatch; ++b) mx = fmaxf(mx, lp[b]);
