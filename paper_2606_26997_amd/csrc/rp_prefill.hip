@@ -127,7 +127,7 @@ constexpr int kKeyBlk = 32;
 // c0 + 4 (s % 4) ... + 3, lane j receives rows r0 .. r0 + 3 of column c0 + j.
 template <int D>
 struct PfSmem {
-  static constexpr int kKPitch = D + 8;   // K rows, bf16 (16-byte aligned rows)
+  static constexpr int kKPitch = D + 16;  // K rows, bf16: the 16-byte reads of 16 rows hit no bank twice
   static constexpr int kVPitch = D + 16;  // V rows, bf16: 4 consecutive rows start 8 banks apart
   static constexpr int kKElems = kKeyBlk * kKPitch;
   static constexpr int kStage = kKElems + kKeyBlk * kVPitch;
@@ -189,10 +189,54 @@ __device__ inline void pf_store(uint16_t* stage, int t, const PfBlock& r) {
   }
 }
 
-// The one-launch prefill of a bf16 pool: the workgroup whose query rows
-// include a key block's first token copies that block's staged K/V rows (the
-// thread's registers, after they went to LDS) into the group's prefix pages.
-// Rows past the prompt's end are not written, as in the page-write kernel.
+// The one-launch prefill of a bf16 pool writes every prompt token's K/V rows
+// into the group's prefix pages from the workgroup whose query rows hold the
+// token (exactly one), in one of two ways; rows past the prompt's end are not
+// written, as in the page-write kernel.
+//
+// With one row tile per wave, the workgroup writes a key block's staged
+// registers (after they went to LDS) when the block starts with one of its
+// tokens. With two row tiles, the page addresses held across the key loop
+// would cost the kernel its third wave per SIMD (178 VGPRs), so the workgroup
+// copies its own rows in the prologue instead: the copy's loads are issued
+// together with the q rows and the first key block, and its stores follow
+// them (1024-token prompts 296 -> 280 us; with one row tile the prologue
+// copy was 5% slower on config-2 prompts, U[64, 512] tokens).
+template <int D, int TPB>
+struct PfOwnRows {
+  static constexpr int kCh = TPB * (D / 8);  // 16-byte pieces of the workgroup's rows (K or V)
+  static constexpr int kPer = (kCh + kPfThreads - 1) / kPfThreads;
+  u32x4_t k[kPer], v[kPer];
+
+  __device__ inline void load(int T0, int last, int t, const uint16_t* kbase, const uint16_t* vbase, uint32_t pitch) {
+    const char* kb = reinterpret_cast<const char*>(kbase);
+    const char* vb = reinterpret_cast<const char*>(vbase);
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+      const int c = t + i * kPfThreads, tok = c / (D / 8), col = (c - tok * (D / 8)) * 8, u = T0 + tok;
+      if (c < kCh && u <= last) {
+        const uint32_t off = ((uint32_t)u * pitch + (uint32_t)col) * 2u;
+        k[i] = *reinterpret_cast<const u32x4_t*>(kb + off);
+        v[i] = *reinterpret_cast<const u32x4_t*>(vb + off);
+      }
+    }
+  }
+
+  __device__ inline void store(const PrefillArgs& a, int g, int h, int T0, int last, int t) const {
+    const int* pbt = a.prefix_block_table + (size_t)g * a.max_prefix_pages;
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+      const int c = t + i * kPfThreads, tok = c / (D / 8), col = (c - tok * (D / 8)) * 8, u = T0 + tok;
+      if (c < kCh && u <= last) {
+        const int page = clamp_page(pbt[u / kPage], a.num_pages);
+        const size_t off = (((size_t)page * a.num_kv_heads + h) * kPage + (u % kPage)) * D + col;
+        *reinterpret_cast<u32x4_t*>(static_cast<uint16_t*>(a.k_pages) + off) = k[i];
+        *reinterpret_cast<u32x4_t*>(static_cast<uint16_t*>(a.v_pages) + off) = v[i];
+      }
+    }
+  }
+};
+
 template <int D>
 __device__ inline void pf_write_pages(const PrefillArgs& a, int g, int h, int u0, int last, int t,
                                       const PfBlock& r) {
@@ -331,7 +375,7 @@ __device__ __forceinline__ void pf_compute(const uint16_t* kst, int u0, int last
 // Register budget: one row tile per wave fits four waves per SIMD (128
 // VGPRs), two row tiles three (168 VGPRs).
 template <int D, int NREP, int RT, bool WP>
-__global__ __launch_bounds__(kPfThreads) __attribute__((amdgpu_waves_per_eu(RT == 1 ? (WP ? 3 : 4) : (WP ? 2 : 3), 8)))
+__global__ __launch_bounds__(kPfThreads) __attribute__((amdgpu_waves_per_eu(RT == 1 ? 4 : 3, 8)))
 void prefill_attn_kernel(const PrefillArgs a, int max_blocks) {
   using L = PfSmem<D>;
   constexpr int KB = D / 32;              // MFMA k-blocks over head_dim
@@ -355,6 +399,10 @@ void prefill_attn_kernel(const PrefillArgs a, int max_blocks) {
   const size_t qpitch = (size_t)Hq * D, kpitch = (size_t)Hkv * D;
   const uint16_t* kbase = static_cast<const uint16_t*>(a.k) + (size_t)first * kpitch + (size_t)h * D;
   const uint16_t* vbase = static_cast<const uint16_t*>(a.v) + (size_t)first * kpitch + (size_t)h * D;
+
+  constexpr bool kOwnCopy = WP && RT == 2, kBlockWrite = WP && RT == 1;
+  PfOwnRows<D, TPB> own;
+  if constexpr (kOwnCopy) own.load(T0, last, t, kbase, vbase, (uint32_t)kpitch);
 
   // Row r16 of row tile rt: token T0 + wave * TPW + rt * TPT + r16 / NREP,
   // query head h * NREP + r16 % NREP. Q is the B operand of S^T = K Q^T.
@@ -387,12 +435,11 @@ void prefill_attn_kernel(const PrefillArgs a, int max_blocks) {
   // The next block's loads are issued before this block's compute and
   // written to the other LDS buffer after it (past the last block they read
   // clamped rows and are never used).
-  // With write_pages, key block b's rows go to the pages from the workgroup
-  // whose rows hold token 32 b (every block of the prompt has exactly one).
   PfBlock nx;
   pf_load<D>(kbase, vbase, (uint32_t)kpitch, 0, last, t, nx);
+  if constexpr (kOwnCopy) own.store(a, g, h, T0, last, t);
   pf_store<D>(smem, t, nx);
-  if (WP && T0 == 0) pf_write_pages<D>(a, g, h, 0, last, t, nx);
+  if (kBlockWrite && T0 == 0) pf_write_pages<D>(a, g, h, 0, last, t, nx);
   __syncthreads();
   for (int blk = 0; blk < nblk; ++blk) {
     pf_load<D>(kbase, vbase, (uint32_t)kpitch, (blk + 1) * kKeyBlk, last, t, nx);
@@ -405,7 +452,7 @@ void prefill_attn_kernel(const PrefillArgs a, int max_blocks) {
                                     qop, oacc, mrow, lrow);
     pf_store<D>(smem + ((blk + 1) & 1) * L::kStage, t, nx);
     const int un = (blk + 1) * kKeyBlk;
-    if (WP && un >= T0 && un < T0 + TPB) pf_write_pages<D>(a, g, h, un, last, t, nx);
+    if (kBlockWrite && un >= T0 && un < T0 + TPB) pf_write_pages<D>(a, g, h, un, last, t, nx);
     __syncthreads();  // the next block is staged; this block's buffer may be overwritten next
   }
 

@@ -81,6 +81,8 @@ CASES = [
     ("long-two-tiles-d128", [400, 700, 513, 385], 16, 8, 128, "bf16"),
     ("long-two-tiles-d64-nrep4", [450, 390, 1], 8, 2, 64, "bf16"),
     ("long-two-tiles-nrep8", [600, 255], 8, 1, 128, "bf16"),
+    ("long-two-tiles-mha", [420, 401, 17], 4, 4, 64, "bf16"),
+    ("long-two-tiles-fp8", [520, 333], 16, 8, 128, "fp8"),
 ]
 
 
