@@ -30,7 +30,11 @@ EXPORTED = ("rp_status_string", "rp_last_error", "rp_kv_append",
             "rp_group_decode_attn_workspace_size", "rp_group_decode_attn", "rp_lse_combine",
             "rp_plan", "rp_attn_parts", "rp_combine_parts", "rp_plan_layout", "rp_validate_layout",
             "rp_prefill_kv_write", "rp_prefill_attn", "rp_decode_qk_prep", "rp_sched_simulate",
-            "rp_grpo_advantage", "rp_prefill", "rp_group_decode_attn_noalloc", "rp_decode_qk_prep_plan")
+            "rp_grpo_advantage", "rp_prefill", "rp_group_decode_attn_noalloc", "rp_decode_qk_prep_plan",
+            "rp_selftest_mfma")
+# include/rp.h rp_selftest_shape: name -> (code, M, N, K)
+RP_SELFTEST_SHAPES = {"16x16x32": (0, 16, 16, 32), "16x16x16": (1, 16, 16, 16), "32x32x16": (2, 32, 32, 16),
+                      "16x16x32_lds_tr": (3, 16, 16, 32), "32x32x16_lds_tr": (4, 32, 32, 16)}
 RP_SCHED_MODES = {"slime": 0, "cgp": 1, "cgp_fgd": 2}
 
 
@@ -117,6 +121,7 @@ def load() -> ctypes.CDLL:
                                                    ctypes.c_size_t, P]),
         "rp_sched_simulate": (ctypes.c_int, [P, P, P, P, P, P, P, P, P, P]),
         "rp_grpo_advantage": (ctypes.c_int, [P, I32, I32, ctypes.c_double, I32, P, P, P, P]),
+        "rp_selftest_mfma": (ctypes.c_int, [I32, P, P, P, P]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -253,6 +258,14 @@ def combine_parts(kv, layout, out, lse, workspace, stream=None) -> None:
     _check(load().rp_combine_parts(ctypes.byref(kv), ctypes.byref(layout), _ptr(out), _ptr(lse),
                                    _ptr(workspace), _ws_bytes(workspace), _stream(stream)),
            "rp_combine_parts")
+
+
+def selftest_mfma(shape, a, b, c, stream=None) -> None:
+    """One MFMA in the kernels' lane layouts: c (fp32 [M][N]) = a (bf16 [M][K]) b (bf16 [K][N]).
+
+    shape: a key of RP_SELFTEST_SHAPES or its integer code."""
+    code = RP_SELFTEST_SHAPES[shape][0] if isinstance(shape, str) else int(shape)
+    _check(load().rp_selftest_mfma(code, _ptr(a), _ptr(b), _ptr(c), _stream(stream)), "rp_selftest_mfma")
 
 
 def lse_combine(o_parts, lse_parts, row_part_offsets, num_rows, head_dim, out, lse_out,

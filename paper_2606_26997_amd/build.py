@@ -12,7 +12,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "librp.so")
 SOURCES = ["rp_api.hip", "rp_plan.hip", "rp_attn.hip", "rp_combine.hip", "rp_append.hip", "rp_prefill.hip",
-           "rp_qkprep.hip", "rp_grpo.hip"]
+           "rp_qkprep.hip", "rp_grpo.hip", "rp_selftest.hip"]
 # Host-only C++ (no device code), built with the system compiler.
 HOST_SOURCES = ["rp_sched.cpp"]
 ARCH = "gfx950"

@@ -707,6 +707,17 @@ rp_status rp_validate_layout(const rp_paged_kv* kv, const rp_group_layout* l, hi
   return RP_OK;
 }
 
+rp_status rp_selftest_mfma(int32_t shape, const void* a, const void* b, float* c, hipStream_t stream) {
+  g_err[0] = 0;
+  if (shape < RP_SELFTEST_MFMA_16X16X32 || shape > RP_SELFTEST_MFMA_32X32X16_LDS_TR)
+    return fail(RP_ERR_UNSUPPORTED, "self-test shape %d unknown", shape);
+  if (a == nullptr || b == nullptr || c == nullptr) return fail(RP_ERR_INVALID_ARG, "a/b/c is NULL");
+  if (!aligned(a, 2) || !aligned(b, 2) || !aligned(c, 4))
+    return fail(RP_ERR_INVALID_ARG, "a and b must be 2-byte and c 4-byte aligned");
+  hipError_t e = rp::launch_selftest_mfma(shape, a, b, c, stream);
+  return e == hipSuccess ? RP_OK : hip_fail(e, "self-test kernel launch");
+}
+
 }  // extern "C"
 
 namespace rp {

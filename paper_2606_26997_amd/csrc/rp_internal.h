@@ -166,5 +166,6 @@ hipError_t launch_prefill_attn(const PrefillArgs& a, int head_dim, int n_rep, hi
 hipError_t launch_qk_prep(QkPrepArgs a, int head_dim, bool fp8, hipStream_t stream);
 hipError_t launch_grpo(const GrpoArgs& a, hipStream_t stream);
 hipError_t launch_validate(const ValidateArgs& a, hipStream_t stream);
+hipError_t launch_selftest_mfma(int shape, const void* a, const void* b, float* c, hipStream_t stream);
 
 }  // namespace rp

@@ -119,12 +119,8 @@ constexpr int kPfThreads = 64 * kPfWaves;
 constexpr int kKeyBlk = 32;
 
 // Both K and V are staged row-major, as they come from the projections. The
-// V^T operand of P V is read with gfx950's transposing LDS read
-// (ds_read_b64_tr_b16): within each 16-lane group, lane s supplies the
-// address of 4 consecutive 16-bit elements, and lane j receives element j % 4
-// of the elements addressed by lanes j / 4, 4 + j / 4, 8 + j / 4 and
-// 12 + j / 4, in that order. With lane s pointing at row r0 + s / 4, columns
-// c0 + 4 (s % 4) ... + 3, lane j receives rows r0 .. r0 + 3 of column c0 + j.
+// V^T operand of P V is read with gfx950's transposing LDS read (lds_read_tr:
+// four rows of one column per lane).
 template <int D>
 struct PfSmem {
   static constexpr int kKPitch = D + 16;  // K rows, bf16: the 16-byte reads of 16 rows hit no bank twice
@@ -256,12 +252,6 @@ __device__ inline void pf_write_pages(const PrefillArgs& a, int g, int h, int u0
   if constexpr (L::kPerThread == 2) put(t + kPfThreads, r.k1, r.v1);
 }
 
-// Four keys of one V column from the row-major staged block (see PfSmem).
-typedef short s16x4_t __attribute__((ext_vector_type(4)));
-__device__ inline bf16x4_t lds_read_tr(const uint16_t* p) {
-  return __builtin_bit_cast(
-      bf16x4_t, __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4_t*)(p)));
-}
 
 // One 32-key block from LDS stage `kst` (keys u0 .. u0 + 31) for this wave's
 // RT row tiles: the scores of both 16-key sub-tiles, the causal mask, one
