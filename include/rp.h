@@ -448,16 +448,14 @@ rp_status rp_sched_simulate(const rp_sched_config* config, const int32_t* prompt
  * and writes the accumulator as c (fp32 [M][N], row-major). With small
  * integer inputs the products are exact, so c must equal a b exactly; any
  * other result means the layouts the kernels rely on do not hold on the
- * device. The _LDS_TR shapes stage a transposed in LDS and read it back
- * with the transposing read, with the key order the prefill uses in P V.
+ * device. The _LDS_TR shape stages a transposed in LDS and reads it back
+ * with the transposing read, in the key order the prefill uses in P V.
  * All pointers are device memory; nothing is allocated. RP_ERR_UNSUPPORTED
  * for an unknown shape, RP_ERR_INVALID_ARG for a NULL or misaligned pointer. */
 typedef enum {
-  RP_SELFTEST_MFMA_16X16X32 = 0,         /* M = N = 16, K = 32 */
-  RP_SELFTEST_MFMA_16X16X16 = 1,         /* M = N = K = 16 */
-  RP_SELFTEST_MFMA_32X32X16 = 2,         /* M = N = 32, K = 16 */
-  RP_SELFTEST_MFMA_16X16X32_LDS_TR = 3,  /* M = N = 16, K = 32 */
-  RP_SELFTEST_MFMA_32X32X16_LDS_TR = 4   /* M = N = 32, K = 16 */
+  RP_SELFTEST_MFMA_16X16X32 = 0,        /* M = N = 16, K = 32 */
+  RP_SELFTEST_MFMA_16X16X16 = 1,        /* M = N = K = 16 */
+  RP_SELFTEST_MFMA_16X16X32_LDS_TR = 2  /* M = N = 16, K = 32 */
 } rp_selftest_shape;
 
 rp_status rp_selftest_mfma(int32_t shape, const void* a, const void* b, float* c, hipStream_t stream);

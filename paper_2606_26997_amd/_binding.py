@@ -33,8 +33,7 @@ EXPORTED = ("rp_status_string", "rp_last_error", "rp_kv_append",
             "rp_grpo_advantage", "rp_prefill", "rp_group_decode_attn_noalloc", "rp_decode_qk_prep_plan",
             "rp_selftest_mfma")
 # include/rp.h rp_selftest_shape: name -> (code, M, N, K)
-RP_SELFTEST_SHAPES = {"16x16x32": (0, 16, 16, 32), "16x16x16": (1, 16, 16, 16), "32x32x16": (2, 32, 32, 16),
-                      "16x16x32_lds_tr": (3, 16, 16, 32), "32x32x16_lds_tr": (4, 32, 32, 16)}
+RP_SELFTEST_SHAPES = {"16x16x32": (0, 16, 16, 32), "16x16x16": (1, 16, 16, 16), "16x16x32_lds_tr": (2, 16, 16, 32)}
 RP_SCHED_MODES = {"slime": 0, "cgp": 1, "cgp_fgd": 2}
 
 

@@ -709,7 +709,7 @@ rp_status rp_validate_layout(const rp_paged_kv* kv, const rp_group_layout* l, hi
 
 rp_status rp_selftest_mfma(int32_t shape, const void* a, const void* b, float* c, hipStream_t stream) {
   g_err[0] = 0;
-  if (shape < RP_SELFTEST_MFMA_16X16X32 || shape > RP_SELFTEST_MFMA_32X32X16_LDS_TR)
+  if (shape < RP_SELFTEST_MFMA_16X16X32 || shape > RP_SELFTEST_MFMA_16X16X32_LDS_TR)
     return fail(RP_ERR_UNSUPPORTED, "self-test shape %d unknown", shape);
   if (a == nullptr || b == nullptr || c == nullptr) return fail(RP_ERR_INVALID_ARG, "a/b/c is NULL");
   if (!aligned(a, 2) || !aligned(b, 2) || !aligned(c, 4))

@@ -59,7 +59,6 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
-typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 __host__ __device__ inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 
@@ -239,21 +238,11 @@ __device__ inline float max_xor16_32(float x) {
   return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
 }
 
-// Max over lanes l and l^32 (the two halves of a 32x32 MFMA tile column).
-__device__ inline float max_xor32(float x) {
-  const uint32_t u = __float_as_uint(x);
-  const auto a = __builtin_amdgcn_permlane32_swap(u, u, false, false);
-  return fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
-}
-
 // MFMA tiles used by the group-prefix and prefill paths (fp32 accumulate).
 // With lane l = 16 q + r (r < 16):
 //   16x16x32 bf16: lane (r, q) supplies A[r][8q..8q+7] and B[8q..8q+7][r];
 //   16x16x16 bf16: lane (r, q) supplies A[r][4q..4q+3] and B[4q..4q+3][r];
 // lane (r, q) receives C[4q..4q+3][r].
-// With lane l = 32 h + n (n < 32):
-//   32x32x16 bf16: lane (n, h) supplies A[n][8h..8h+7] and B[8h..8h+7][n];
-// entry i of lane (n, h) receives C[8 (i / 4) + 4 h + i % 4][n].
 // rp_selftest_mfma checks each of these against a matrix product.
 __device__ inline f32x4_t mfma16x16x32(const bf16x8_t& a, const bf16x8_t& b, const f32x4_t& c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
@@ -262,10 +251,6 @@ __device__ inline f32x4_t mfma16x16x16(const bf16x4_t& a, const bf16x4_t& b, con
   typedef short s16x4_t __attribute__((ext_vector_type(4)));
   return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4_t, a), __builtin_bit_cast(s16x4_t, b),
                                                    c, 0, 0, 0);
-}
-
-__device__ inline f32x16_t mfma32x32x16(const bf16x8_t& a, const bf16x8_t& b, const f32x16_t& c) {
-  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
 // gfx950's transposing LDS read (ds_read_b64_tr_b16): within each 16-lane

@@ -13,7 +13,7 @@ namespace {
 typedef unsigned short u16x8_t __attribute__((ext_vector_type(8)));
 typedef unsigned short u16x4_t __attribute__((ext_vector_type(4)));
 
-constexpr int kTrPitch = 48;  // staged A^T rows (bf16), 8-byte aligned rows
+constexpr int kTrPitch = 32;  // staged A^T rows (bf16), 8-byte aligned rows
 
 // bf16 elements src[idx(0)] .. src[idx(7)] as an MFMA operand.
 template <class F>
@@ -26,10 +26,9 @@ __device__ inline bf16x8_t gather8(const uint16_t* src, F idx) {
 
 __global__ __launch_bounds__(64) void selftest_mfma_kernel(int shape, const uint16_t* a, const uint16_t* b,
                                                            float* c) {
-  __shared__ __attribute__((aligned(16))) uint16_t at[32 * kTrPitch];
+  __shared__ __attribute__((aligned(16))) uint16_t at[32 * kTrPitch];  // A^T, 32 keys x 16 columns
   const int l = threadIdx.x;
   const int r = l & 15, q = l >> 4;  // 16x16 tiles: lane (r, q)
-  const int n = l & 31, h = l >> 5;  // 32x32 tiles: lane (n, h)
   if (shape == RP_SELFTEST_MFMA_16X16X32) {
     constexpr int K = 32, N = 16;
     const bf16x8_t av = gather8(a, [&](int j) { return r * K + 8 * q + j; });
@@ -49,14 +48,6 @@ __global__ __launch_bounds__(64) void selftest_mfma_kernel(int shape, const uint
                                      f32x4_t{0.f, 0.f, 0.f, 0.f});
 #pragma unroll
     for (int i = 0; i < 4; ++i) c[(4 * q + i) * N + r] = acc[i];
-  } else if (shape == RP_SELFTEST_MFMA_32X32X16) {
-    constexpr int K = 16, N = 32;
-    const bf16x8_t av = gather8(a, [&](int j) { return n * K + 8 * h + j; });
-    const bf16x8_t bv = gather8(b, [&](int j) { return (8 * h + j) * N + n; });
-    f32x16_t acc = {};
-    acc = mfma32x32x16(av, bv, acc);
-#pragma unroll
-    for (int i = 0; i < 16; ++i) c[(8 * (i / 4) + 4 * h + i % 4) * N + n] = acc[i];
   } else if (shape == RP_SELFTEST_MFMA_16X16X32_LDS_TR) {
     // The prefill's P V with 16x16 tiles: A^T (keys x columns) staged
     // row-major; lane (r, q) takes column r of keys 4q .. 4q+3 and
@@ -71,22 +62,6 @@ __global__ __launch_bounds__(64) void selftest_mfma_kernel(int shape, const uint
     const f32x4_t acc = mfma16x16x32(av, bv, f32x4_t{0.f, 0.f, 0.f, 0.f});
 #pragma unroll
     for (int i = 0; i < 4; ++i) c[(4 * q + i) * N + r] = acc[i];
-  } else if (shape == RP_SELFTEST_MFMA_32X32X16_LDS_TR) {
-    // The prefill's P V with 32x32 tiles: lane (n, h) takes column n of keys
-    // 4h .. 4h+3 and 8+4h .. 8+4h+3 (the 16-lane group of lanes 16-31 and
-    // 48-63 reads columns 16-31), the key order of a 32x32 score tile.
-    constexpr int M = 32, K = 16, N = 32;
-    for (int i = l; i < M * K; i += 64) at[(i % K) * kTrPitch + i / K] = a[i];
-    __syncthreads();
-    const int s = l & 15;
-    const uint16_t* p = at + (4 * h + s / 4) * kTrPitch + ((l >> 4) & 1) * 16 + 4 * (s % 4);
-    const bf16x4_t a0 = lds_read_tr(p), a1 = lds_read_tr(p + 8 * kTrPitch);
-    const bf16x8_t av = __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7);
-    const bf16x8_t bv = gather8(b, [&](int j) { return (j < 4 ? 4 * h + j : 4 + 4 * h + j) * N + n; });
-    f32x16_t acc = {};
-    acc = mfma32x32x16(av, bv, acc);
-#pragma unroll
-    for (int i = 0; i < 16; ++i) c[(8 * (i / 4) + 4 * h + i % 4) * N + n] = acc[i];
   }
 }
 

@@ -19,7 +19,7 @@ def _bf16(x):
     return torch.from_numpy(x.astype(np.float32)).to(torch.bfloat16)
 
 
-@pytest.mark.parametrize("shape", ["16x16x32", "16x16x16", "32x32x16", "16x16x32_lds_tr", "32x32x16_lds_tr"])
+@pytest.mark.parametrize("shape", ["16x16x32", "16x16x16", "16x16x32_lds_tr"])
 @pytest.mark.parametrize("seed", [0, 1])
 def test_one_mfma_equals_the_matrix_product(shape, seed):
     import paper_2606_26997_amd as rp
