@@ -266,15 +266,21 @@ def copy_calibration(steps):
 
 
 def read_ceiling(steps):
-    """Context for the roofline: plain streaming kernels of torch on this GPU, median over steps.
-    A 4 GiB sum (read only) and a 1 GiB copy (read + write); both exceed the 256 MB last-level cache."""
+    """Context for the roofline, median over steps: the library's streaming-read probe (plain and
+    non-temporal loads) and torch's own streaming kernels on this GPU. A 4 GiB read and sum, and
+    a 1 GiB copy (read + write); all exceed the 256 MB last-level cache."""
     import numpy as np
     import torch
+    import paper_2606_26997_amd as rp
     x = torch.ones(1 << 31, dtype=torch.bfloat16, device="cuda")      # 4 GiB
     a = torch.ones(1 << 30, dtype=torch.uint8, device="cuda")
     b = torch.empty_like(a)
+    sink = torch.zeros(rp.RP_STREAM_READ_SINK_WORDS, dtype=torch.int32, device="cuda")
+    xb = x.numel() * 2
     res = {}
-    for name, fn, nbytes in (("sum_read", lambda: x.sum(dtype=torch.float32), x.numel() * 2),
+    for name, fn, nbytes in (("rp_stream_read", lambda: rp.stream_read(x, xb, sink), xb),
+                             ("rp_stream_read_nontemporal", lambda: rp.stream_read(x, xb, sink, nontemporal=True), xb),
+                             ("sum_read", lambda: x.sum(dtype=torch.float32), xb),
                              ("copy_read_write", lambda: b.copy_(a), 2 * a.numel())):
         for _ in range(3):
             fn()

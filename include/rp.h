@@ -460,6 +460,20 @@ typedef enum {
 
 rp_status rp_selftest_mfma(int32_t shape, const void* a, const void* b, float* c, hipStream_t stream);
 
+/* ---- Streaming-read probe ----
+ * Measurement infrastructure: the HBM read rate a plain kernel reaches on
+ * this device, the practical ceiling for the memory-bound decode kernels
+ * (bench.py --read-ceiling times it). Reads `bytes` bytes at src once with
+ * 16-byte vector loads spread over RP_STREAM_READ_BLOCKS workgroups, with the
+ * non-temporal load hint when nontemporal != 0 (as the decode kernel's V
+ * stream), and writes RP_STREAM_READ_SINK_WORDS folded words to sink so that
+ * no load can be dropped. src: device memory, 16-byte aligned, bytes a
+ * multiple of 16; sink: device memory, 4-byte aligned. Nothing is allocated.
+ * RP_ERR_INVALID_ARG for a NULL or misaligned pointer or a bad size. */
+#define RP_STREAM_READ_BLOCKS 2048
+#define RP_STREAM_READ_SINK_WORDS (RP_STREAM_READ_BLOCKS * 4)
+rp_status rp_stream_read(const void* src, uint64_t bytes, uint32_t* sink, int32_t nontemporal, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

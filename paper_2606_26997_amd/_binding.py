@@ -31,7 +31,8 @@ EXPORTED = ("rp_status_string", "rp_last_error", "rp_kv_append",
             "rp_plan", "rp_attn_parts", "rp_combine_parts", "rp_plan_layout", "rp_validate_layout",
             "rp_prefill_kv_write", "rp_prefill_attn", "rp_decode_qk_prep", "rp_sched_simulate",
             "rp_grpo_advantage", "rp_prefill", "rp_group_decode_attn_noalloc", "rp_decode_qk_prep_plan",
-            "rp_selftest_mfma")
+            "rp_selftest_mfma", "rp_stream_read")
+RP_STREAM_READ_SINK_WORDS = 2048 * 4   # include/rp.h
 # include/rp.h rp_selftest_shape: name -> (code, M, N, K)
 RP_SELFTEST_SHAPES = {"16x16x32": (0, 16, 16, 32), "16x16x16": (1, 16, 16, 16), "16x16x32_lds_tr": (2, 16, 16, 32)}
 RP_SCHED_MODES = {"slime": 0, "cgp": 1, "cgp_fgd": 2}
@@ -121,6 +122,7 @@ def load() -> ctypes.CDLL:
         "rp_sched_simulate": (ctypes.c_int, [P, P, P, P, P, P, P, P, P, P]),
         "rp_grpo_advantage": (ctypes.c_int, [P, I32, I32, ctypes.c_double, I32, P, P, P, P]),
         "rp_selftest_mfma": (ctypes.c_int, [I32, P, P, P, P]),
+        "rp_stream_read": (ctypes.c_int, [P, ctypes.c_uint64, P, I32, P]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -265,6 +267,12 @@ def selftest_mfma(shape, a, b, c, stream=None) -> None:
     shape: a key of RP_SELFTEST_SHAPES or its integer code."""
     code = RP_SELFTEST_SHAPES[shape][0] if isinstance(shape, str) else int(shape)
     _check(load().rp_selftest_mfma(code, _ptr(a), _ptr(b), _ptr(c), _stream(stream)), "rp_selftest_mfma")
+
+
+def stream_read(src, nbytes, sink, nontemporal=False, stream=None) -> None:
+    """Read nbytes of device tensor src once (16-byte loads); sink: int32/uint32 [RP_STREAM_READ_SINK_WORDS]."""
+    _check(load().rp_stream_read(_ptr(src), int(nbytes), _ptr(sink), int(bool(nontemporal)), _stream(stream)),
+           "rp_stream_read")
 
 
 def lse_combine(o_parts, lse_parts, row_part_offsets, num_rows, head_dim, out, lse_out,

@@ -718,6 +718,15 @@ rp_status rp_selftest_mfma(int32_t shape, const void* a, const void* b, float* c
   return e == hipSuccess ? RP_OK : hip_fail(e, "self-test kernel launch");
 }
 
+rp_status rp_stream_read(const void* src, uint64_t bytes, uint32_t* sink, int32_t nontemporal, hipStream_t stream) {
+  g_err[0] = 0;
+  if (src == nullptr || sink == nullptr) return fail(RP_ERR_INVALID_ARG, "src/sink is NULL");
+  if (!aligned(src, 16) || !aligned(sink, 4)) return fail(RP_ERR_INVALID_ARG, "src must be 16-byte and sink 4-byte aligned");
+  if (bytes == 0 || bytes % 16 != 0) return fail(RP_ERR_INVALID_ARG, "bytes must be a positive multiple of 16");
+  hipError_t e = rp::launch_stream_read(src, bytes, sink, nontemporal != 0, stream);
+  return e == hipSuccess ? RP_OK : hip_fail(e, "stream-read kernel launch");
+}
+
 }  // extern "C"
 
 namespace rp {

@@ -167,5 +167,7 @@ hipError_t launch_qk_prep(QkPrepArgs a, int head_dim, bool fp8, hipStream_t stre
 hipError_t launch_grpo(const GrpoArgs& a, hipStream_t stream);
 hipError_t launch_validate(const ValidateArgs& a, hipStream_t stream);
 hipError_t launch_selftest_mfma(int shape, const void* a, const void* b, float* c, hipStream_t stream);
+hipError_t launch_stream_read(const void* src, uint64_t bytes, uint32_t* sink, bool nontemporal,
+                              hipStream_t stream);
 
 }  // namespace rp

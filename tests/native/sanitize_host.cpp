@@ -157,6 +157,8 @@ void validation() {
   EXPECT(rp_grpo_advantage(nullptr, 0, 8, 1e-6, 1, nullptr, nullptr, nullptr, nullptr) == RP_OK);
   EXPECT(rp_selftest_mfma(9, A, A, static_cast<float*>(A), nullptr) == RP_ERR_UNSUPPORTED);
   EXPECT(rp_selftest_mfma(0, nullptr, A, static_cast<float*>(A), nullptr) == RP_ERR_INVALID_ARG);
+  EXPECT(rp_stream_read(A, 24, static_cast<uint32_t*>(A), 0, nullptr) == RP_ERR_INVALID_ARG);
+  EXPECT(rp_stream_read(nullptr, 1024, static_cast<uint32_t*>(A), 1, nullptr) == RP_ERR_INVALID_ARG);
   rp_prefill_layout pl{2, 4, 10, static_cast<const int32_t*>(A), static_cast<const int32_t*>(A), 2};
   EXPECT(rp_prefill_kv_write(&kv, &pl, nullptr, A, nullptr) == RP_ERR_INVALID_ARG);
   EXPECT(rp_prefill_attn(&kv, &pl, A, A, A, 0.0f, A, nullptr, nullptr) == RP_ERR_INVALID_ARG);

@@ -266,6 +266,16 @@ def test_selftest_mfma_argument_checks():
     assert sorted(code for code, *_ in rp.RP_SELFTEST_SHAPES.values()) == [0, 1, 2]
 
 
+def test_stream_read_argument_checks():
+    lib = rp.load()
+    call = lambda src=A, n=1 << 20, sink=A, nt=0: lib.rp_stream_read(src, n, sink, nt, None)
+    assert call(src=None) == rp.RP_ERR_INVALID_ARG and "NULL" in rp.last_error()
+    assert call(src=A + 8) == rp.RP_ERR_INVALID_ARG and "aligned" in rp.last_error()
+    assert call(sink=A + 2) == rp.RP_ERR_INVALID_ARG
+    assert call(n=0) == rp.RP_ERR_INVALID_ARG and "multiple of 16" in rp.last_error()
+    assert call(n=24) == rp.RP_ERR_INVALID_ARG
+
+
 def _no_gpu():
     import torch
     return not torch.cuda.is_available()
