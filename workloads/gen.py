@@ -89,16 +89,37 @@ class Workload:
         return 1 if self.kv_dtype == "fp8" else 2
 
 
+# The casts run on the generator's worker threads. Casting through torch in
+# large pieces would start an OpenMP thread team per worker thread, and a
+# process holding such teams cannot safely fork afterwards (the oracle's CPU
+# baseline forks its workers from the process that generated the workload:
+# the forked workers were seen to block forever in the unwinder's lock). So
+# bf16 rounding is done in numpy, and the fp8 cast goes through torch in
+# pieces below ATen's parallel grain (32768 elements), which run on the
+# calling thread alone.
+_CAST_PIECE = 16384
+
+
 def _to_bf16_bits(x: np.ndarray) -> np.ndarray:
-    import torch
-    t = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).to(torch.bfloat16)
-    return t.view(torch.int16).numpy().view(np.uint16)
+    """float32 -> bf16 bit patterns, rounded to nearest even (NaN -> a quiet NaN of the same sign)."""
+    f = np.ascontiguousarray(x, dtype=np.float32)
+    u = f.view(np.uint32)
+    r = ((u + (np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1)))) >> np.uint32(16)).astype(np.uint16)
+    nan = np.isnan(f)
+    if nan.any():
+        r[nan] = ((u[nan] >> np.uint32(16)) | np.uint32(0x0040)).astype(np.uint16)
+    return r
 
 
 def _to_e4m3_codes(x: np.ndarray) -> np.ndarray:
     import torch
-    t = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).to(torch.float8_e4m3fn)
-    return t.view(torch.uint8).numpy()
+    f = np.ascontiguousarray(x, dtype=np.float32)
+    flat = f.reshape(-1)
+    out = np.empty(flat.shape, dtype=np.uint8)
+    for i in range(0, flat.size, _CAST_PIECE):
+        t = torch.from_numpy(flat[i:i + _CAST_PIECE]).to(torch.float8_e4m3fn)
+        out[i:i + _CAST_PIECE] = t.view(torch.uint8).numpy()
+    return out.reshape(f.shape)
 
 
 def _workers() -> int:
