@@ -294,44 +294,7 @@ def read_ceiling(steps):
         ms = float(np.median([e0.elapsed_time(e1) for e0, e1 in ev]))
         res[name] = {"bytes": nbytes, "ms": round(ms, 4), "GBps": round(nbytes / ms / 1e6, 1),
                      "frac_of_8TBps": round(nbytes / ms / 1e6 / HBM_PEAK_GBPS, 4)}
-    del x, a, b, sink
-    torch.cuda.empty_cache()
-    for kn, vn in ((False, True), (True, True), (False, False)):
-        for npu in (128, 32):
-            name = f"rp_paged_read_k{'nt' if kn else 'plain'}_v{'nt' if vn else 'plain'}_{npu}pages"
-            gbps = paged_read_ceiling(steps, kn, vn, npu)
-            res[name] = {"bytes": 2 * (1 << 19) * 4096, "GBps": gbps, "frac_of_8TBps": round(gbps / HBM_PEAK_GBPS, 4)}
     print(json.dumps({"read_ceiling": res}), flush=True)
-
-
-def paged_read_ceiling(steps=10, k_nt=False, v_nt=True, pages_per_unit=128):
-    """The decode kernel's access pattern without its arithmetic (rp_paged_read): two 2 GiB pools of
-    4 KiB (page, kv-head) blocks, each visited once through a seeded random permutation, units of
-    pages_per_unit pages, one wave each; median of steps, GB/s."""
-    import numpy as np
-    import torch
-    import paper_2606_26997_amd as rp
-    nblocks = 1 << 19
-    k = torch.empty(nblocks * 4096, dtype=torch.uint8, device="cuda")
-    v = torch.empty_like(k)
-    k.fill_(1)
-    v.fill_(2)
-    table = torch.from_numpy(np.random.default_rng(4096).permutation(nblocks).astype(np.int32)).cuda()
-    units = nblocks // pages_per_unit
-    sink = torch.zeros(units, dtype=torch.int32, device="cuda")
-    run = lambda: rp.paged_read(k, v, table, units, pages_per_unit, sink, k_nontemporal=k_nt, v_nontemporal=v_nt)
-    for _ in range(2):
-        run()
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
-    for e0, e1 in ev:
-        e0.record()
-        run()
-        e1.record()
-    torch.cuda.synchronize()
-    ms = float(np.median([e0.elapsed_time(e1) for e0, e1 in ev]))
-    del k, v, table, sink
-    torch.cuda.empty_cache()
-    return round(2 * nblocks * 4096 / ms / 1e6, 1)
 
 
 def stream_read_ceiling(steps=10):
@@ -857,9 +820,7 @@ def main():
 
     # Phase 2: the GPU, one workload at a time, after the practical read ceiling.
     args.read_ceiling_gbps = stream_read_ceiling()
-    args.pattern_ceiling_gbps = paged_read_ceiling()
-    print(f"[bench] read ceilings: streaming {args.read_ceiling_gbps} GB/s, decode access pattern "
-          f"{args.pattern_ceiling_gbps} GB/s", file=sys.stderr, flush=True)
+    print(f"[bench] streaming-read ceiling: {args.read_ceiling_gbps} GB/s", file=sys.stderr, flush=True)
     for i, (cfg, wl, cpu) in enumerate(prepared):
         line = decode_bench(cfg, wl, cpu, args)
         prepared[i] = None
@@ -931,12 +892,8 @@ def decode_bench(cfg, wl, cpu, args):
     achieved = bm["parts_kernel"] / (parts_us * 1e-6) / 1e9
     traffic = load_traffic(f"config{cfg.cid}") if args.seed is None else None
     rc = getattr(args, "read_ceiling_gbps", None)
-    pc = getattr(args, "pattern_ceiling_gbps", None)
-    # Context, not the roofline's peak: the kernel's rate against what a plain streaming read reaches,
-    # and against its own access pattern (scattered 4 KiB K/V blocks) read with no arithmetic.
-    ceiling = {"GBps": rc, "frac": round(achieved / rc, 4), "probe": "rp_stream_read, 4 GiB, non-temporal loads",
-               "pattern_GBps": pc, "pattern_frac": round(achieved / pc, 4) if pc else None,
-               "pattern_probe": "rp_paged_read, 2 x 2 GiB of 4 KiB blocks, random order, 128-page units"} \
+    # Context, not the roofline's peak: the kernel's rate against what a plain streaming read reaches.
+    ceiling = {"GBps": rc, "frac": round(achieved / rc, 4), "probe": "rp_stream_read, 4 GiB, non-temporal loads"} \
         if rc else None
     return {
         "metric": METRIC,
