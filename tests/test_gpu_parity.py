@@ -377,7 +377,7 @@ RANDOM = [(11, None), (22, None), (33, None), (44, None), (55, None), (66, None)
 
 @pytest.mark.timeout(600)
 @pytest.mark.parametrize("seed,big", RANDOM, ids=[str(r[0]) for r in RANDOM])
-def test_random_batches_sampled_rows(seed, big):
+def test_random_batches_every_row(seed, big):
     """Random shapes across the kernel templates (n_rep, head_dim, kv dtype) and piece lengths; every
     sequence is compared with the oracle."""
     kw = _random_case(seed, big)
