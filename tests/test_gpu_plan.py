@@ -159,6 +159,22 @@ def _case(name):
         G, S = 3, 10
         s2g = rng.integers(0, G, S)
         P, L = np.zeros(G, int), np.zeros(S, int)
+    elif name == "mid-65":                 # just past the single-wave planner's 64 sequences
+        G, S = 9, 65
+        s2g = rng.integers(0, G, S)
+        P, L = rng.integers(0, 600, G), rng.integers(0, 5000, S)
+    elif name == "mid-100-many-groups":    # general planner, many groups without members
+        G, S = 300, 100
+        s2g = rng.integers(0, G, S)
+        P, L = rng.integers(0, 700, G), rng.integers(0, 3000, S)
+    elif name == "mid-256-equal-lengths":  # ties among all the last pieces
+        G, S = 32, 256
+        s2g = rng.permutation(np.repeat(np.arange(G), 8))
+        P, L = rng.integers(1, 200, G), np.full(S, 1000)
+    elif name == "mid-200-all-empty":      # no prefix, no response tokens
+        G, S = 7, 200
+        s2g = rng.integers(0, G, S)
+        P, L = np.zeros(G, int), np.zeros(S, int)
     else:
         raise KeyError(name)
     return G, s2g, P, L
@@ -167,7 +183,8 @@ def _case(name):
 CASES = ["qwen-layer-uniform", "lognormal-tail", "frontier-random-map", "long-context", "many-sequences",
          "many-pieces", "frontier-dispatch-16", "frontier-dispatch-64", "frontier-dispatch-64-long",
          "few-long-sequences", "empty-and-idle-groups", "small-many-groups", "small-equal-lengths",
-         "single-sequence", "small-all-empty"]
+         "single-sequence", "small-all-empty", "mid-65", "mid-100-many-groups", "mid-256-equal-lengths",
+         "mid-200-all-empty"]
 
 
 @pytest.mark.parametrize("name", CASES)
@@ -180,7 +197,8 @@ def test_plan_matches_its_contract(name):
     if torch.cuda.get_device_properties(0).multi_processor_count == 256:   # MI355X: every candidate B occurs
         want = {"frontier-dispatch-16": 16, "few-long-sequences": 16, "empty-and-idle-groups": 16,
                 "frontier-dispatch-64": 64, "frontier-dispatch-64-long": 96, "small-many-groups": 16,
-                "small-equal-lengths": 16, "single-sequence": 16, "small-all-empty": 16}.get(name, 128)
+                "small-equal-lengths": 16, "single-sequence": 16, "small-all-empty": 16, "mid-65": 64,
+                "mid-100-many-groups": 32, "mid-256-equal-lengths": 96, "mid-200-all-empty": 16}.get(name, 128)
         assert B == want, (name, B)
     # A second plan into the same workspace gives the same B-page items.
     check_plan(b, s2g, P, L, rbt, G)
