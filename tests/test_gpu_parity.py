@@ -236,6 +236,49 @@ def test_shared_prefix_equals_duplicated_prefix_on_gpu():
     assert np.abs(l1 - l2).max() <= 1e-4
 
 
+def test_logical_key_order_permutation_within_tolerance():
+    # Attention over a set of keys does not depend on their order: the same
+    # keys in another logical order (prefix and response rows shuffled, so
+    # pieces, chunks and page boundaries all change) give the same result up
+    # to rounding.
+    _say("logical key order permutation")
+    rng = np.random.default_rng(21)
+    S, G = 12, 3
+    P, L = [90, 33, 160], list(rng.integers(1, 700, size=S))
+    pk, pv, rk, rv, s2g, q = random_dense(rng, S=S, G=G, Hq=16, Hkv=8, d=128, prefix_lens=P, resp_lens=L)
+    perm_p = [rng.permutation(len(x)) for x in pk]
+    perm_r = [rng.permutation(len(x)) for x in rk]
+    wl1 = paged_from_dense(pk, pv, rk, rv, s2g, q, num_kv_heads=8, seed=5)
+    wl2 = paged_from_dense([x[i] for x, i in zip(pk, perm_p)], [x[i] for x, i in zip(pv, perm_p)],
+                           [x[i] for x, i in zip(rk, perm_r)], [x[i] for x, i in zip(rv, perm_r)],
+                           s2g, q, num_kv_heads=8, seed=6)
+    _, o1, l1 = run_hip(wl1)
+    _, o2, l2 = run_hip(wl2)
+    assert np.abs(o1 - o2).max() <= 1e-2
+    assert np.abs(l1 - l2).max() <= 1e-4
+    ref_out, ref_lse = oracle.attention_for_workload(wl1)
+    compare(o2, l2, ref_out, ref_lse, "bf16", "permuted keys")
+
+
+def test_gqa_mapping_value_in_one_kv_head():
+    # V nonzero in kv-head 3 only: exactly query heads 6 and 7 (n_rep = 2,
+    # q-head j reads kv-head j // 2) have a nonzero output; every other
+    # head's output is exactly zero.
+    _say("GQA mapping, V in one kv-head")
+    rng = np.random.default_rng(22)
+    S, G, h = 8, 2, 3
+    P, L = [40, 77], list(rng.integers(0, 300, size=S))
+    pk, pv, rk, rv, s2g, q = random_dense(rng, S=S, G=G, Hq=16, Hkv=8, d=128, prefix_lens=P, resp_lens=L)
+    keep = lambda x: np.where((np.arange(8) == h)[None, :, None], x, np.uint16(0))
+    wl = paged_from_dense(pk, [keep(x) for x in pv], rk, [keep(x) for x in rv], s2g, q, num_kv_heads=8, seed=7)
+    _, out, lse = run_hip(wl)
+    others = [j for j in range(16) if j // 2 != h]
+    assert np.all(out[:, others] == 0)
+    assert np.all(np.abs(out[:, [2 * h, 2 * h + 1]]).max(axis=2) > 0)
+    ref_out, ref_lse = oracle.attention_for_workload(wl)
+    compare(out, lse, ref_out, ref_lse, "bf16", "one kv-head")
+
+
 def test_fp8_all_codes_decode_like_the_oracle():
     """A single key: out = decoded V codes * v_scale exactly (bf16 holds every e4m3 value)."""
     _say("fp8 256 codes")
