@@ -87,10 +87,9 @@ def test_binary_rewards_bitwise(K):
     assert same.any() and np.all(got[0][same] == 0.0)
 
 
-def test_large_batch_sampled():
+def test_large_batch_every_group():
     _say("grpo 2^20 groups")
     R, K = 1 << 20, 8
     r = np.random.default_rng(5).standard_normal((R, K)).astype(np.float32)
     adv, mu, sd = _run(r)
-    idx = np.random.default_rng(6).choice(R, 4096, replace=False)
-    _check((adv[idx], mu[idx], sd[idx]), oracle.advantage_f32(r[idx]), "2^20 sampled")
+    _check((adv, mu, sd), oracle.advantage_f32(r), "2^20 groups")
