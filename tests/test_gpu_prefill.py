@@ -116,6 +116,25 @@ def test_qwen_layer_prompts_full(one_call):
     _check_attn(b, w, "qwen-prompts")
 
 
+@pytest.mark.timeout(300)
+@pytest.mark.parametrize("one_call", [False, True], ids=["two-calls", "rp_prefill"])
+def test_1024_token_prompts_full(one_call):
+    # The prefill bench's long case: 32 groups of 1024-token prompts (two
+    # row tiles per wave; rp_prefill copies each workgroup's own rows into the
+    # pages in its prologue), every row against the oracle.
+    import paper_2606_26997_amd as rp
+    _say(f"prefill 32 groups x 1024 tokens, {'rp_prefill' if one_call else 'two calls'}")
+    w = make_prefill_workload(num_q_heads=16, num_kv_heads=8, head_dim=128, prefix_lens=[1024] * 32, seed=1024)
+    if one_call:
+        b = rp.PrefillBatch.from_workload(w)
+        b.prefill()
+        torch.cuda.synchronize()
+    else:
+        b = _run(w)
+    _check_pages(b, w, "1024-token prompts")
+    _check_attn(b, w, "1024-token prompts")
+
+
 def test_long_prompts():
     # Largest prompts of the tests: a 4096-token prompt (256 prefix pages) and a
     # ragged 2200-token one; 128 key blocks for the last rows.
