@@ -187,14 +187,18 @@ def test_qk_prep_slot_outside_table_gets_q_but_no_append():
     _check_pool(b, wl, x, _bits(b.k_out), kb, "slot outside the table", seqs=[0, 2])
 
 
+@pytest.mark.parametrize("S", [1100, 4096])
 @pytest.mark.parametrize("kv_dtype", ["bf16", "fp8"])
-def test_qk_prep_large_batch_one_block_per_sequence(kv_dtype):
-    # From 1024 sequences on, one block covers all heads of a sequence.
-    _say(f"qk prep 1100 sequences {kv_dtype}")
-    rng = np.random.default_rng(99)
-    S, G = 1100, 140
+def test_qk_prep_large_batch_one_block_per_sequence(kv_dtype, S):
+    # From 1024 sequences on, one block covers all heads of a sequence; 4096
+    # sequences of one response page each is the prep-only launch of the
+    # frontier bench.
+    _say(f"qk prep {S} sequences {kv_dtype}")
+    rng = np.random.default_rng(99 + S)
+    G = S // 8
     s2g = rng.integers(0, G, S)
-    wl, x, b = _setup(s2g, rng.integers(0, 64, G), rng.integers(0, 40, S), 16, 8, 128, kv_dtype, seed=31)
+    wl, x, b = _setup(s2g, rng.integers(0, 64, G), rng.integers(0, 16 if S == 4096 else 40, S), 16, 8, 128,
+                      kv_dtype, seed=31)
     b.set_projections(x.q_in, x.k_in, x.v_in, x.q_norm_w, x.k_norm_w, keep_k=True)
     b.qk_prep()
     torch.cuda.synchronize()
@@ -202,7 +206,7 @@ def test_qk_prep_large_batch_one_block_per_sequence(kv_dtype):
     _check_bits(_bits(b.q), qb, "q")
     k_gpu = _bits(b.k_out)
     _check_bits(k_gpu, kb, "k")
-    _check_pool(b, wl, x, k_gpu, kb, f"1100 sequences {kv_dtype}")
+    _check_pool(b, wl, x, k_gpu, kb, f"{S} sequences {kv_dtype}")
 
 
 @pytest.mark.parametrize("kv_dtype", ["bf16", "fp8"])
